@@ -1,0 +1,345 @@
+"""CPU oracle of the policy-masked MoE layer forward.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the package smoke check and the
+benchmark's CPU-baseline leg may import this module. It shares no code with the
+HIP path and must never be used to produce the library's results.
+
+It is a plain, slow, fp64 definition of what one policy-masked MoE layer
+computes, following Policy-Masked Private Experts (arXiv 2608.06690):
+
+* resolve    trusted metadata -> tau in {0, 1}, failing closed
+             (Sec. 3.1, resolver paragraph; App. B.1 "Policy resolution and masked routing")
+* words      tau per request compiled to one 32-bit policy word and expanded per
+             token row (App. B.1, second paragraph; App. B.2); on the device side a
+             word allows only if it equals ALLOW_WORD exactly
+* route      router logits z = x . W_r[e] (+ b_e) over the permitted pool, the hard
+             mask m(tau) of Sec. 3.1 (mask equation) applied BEFORE top-k, top-k with
+             the lowest expert id winning fp32 ties, gates
+* dispatch   stable grouping of the selected (token, expert) pairs by expert
+* experts    bias-free SwiGLU experts (gate, up, down projections as named in
+             Sec. 4.2 "Matched adaptation and controls"); private experts are run by a
+             separate function that counts the rows it executes, like the
+             independent forward hooks of App. F.1
+* combine    out_t = sum_j g_tj * y_{e_tj}(x_t) (+ shared experts)
+* audit      per-request private rows, deny violations (App. B.2 "route counters
+             indexed by row and layer"; App. F.1)
+
+Readings where the paper is silent (the paper gives only the mask and top-k):
+
+* Gates: RENORM (softmax over the k selected logits, i.e. pool softmax followed by
+  top-k renormalisation) or POOL_SOFTMAX (softmax over the whole permitted pool,
+  no renormalisation).
+* Logits are fp32: the fp64 dot product of the exact inputs rounded once to fp32;
+  a bias is then added in fp32.
+* Ties: equal fp32 logits are broken by the lower expert id; -0.0 equals +0.0;
+  a NaN logit ranks as -inf.
+* The selected ids of a token are reported in ascending id order, with their
+  gates aligned.
+* Shared experts are always executed, independent of tau, added unweighted and
+  never counted by the audit.
+* Expert math is exact fp64 on the (fp32 or bf16) input values with no
+  intermediate rounding.
+
+Parity of the floating-point expert outputs is pinned only by special cases (a
+one-expert pool reduces to a dense SwiGLU MLP; all-deny equals a plain public-only
+top-k MoE); the paper prints no numeric worked example of the layer.
+"""
+from __future__ import annotations
+
+from collections.abc import Mapping
+from dataclasses import dataclass, field
+from typing import Any, Dict, List, Optional, Sequence
+
+import numpy as np
+
+ALLOW_WORD = 0xA11C0DE5   # the only policy word that allows
+DENY_WORD = 0x00000000
+
+GATE_RENORM = "renorm"
+GATE_POOL_SOFTMAX = "pool_softmax"
+
+NEAR_TIE = 1e-5
+
+
+# ----------------------------------------------------------------------------
+# Policy resolution (Sec. 3.1 resolver paragraph; App. B.1)
+# ----------------------------------------------------------------------------
+
+def resolve(meta: Any) -> int:
+    """tau = 1 only for a trusted mapping whose 'allow_private' value has Boolean type
+    and is true. Missing metadata, wrong keys, strings, numbers, lists, nested values,
+    nulls and serialized JSON text all resolve to 0 (fail closed)."""
+    if not isinstance(meta, Mapping):
+        return 0
+    if "allow_private" not in meta:
+        return 0
+    v = meta["allow_private"]
+    if type(v) is bool and v is True:
+        return 1
+    return 0
+
+
+def compile_words(metas: Sequence[Any], lengths: Sequence[int]) -> np.ndarray:
+    """Per-token policy words: each request's resolved decision, repeated over its rows
+    (App. B.1: the resolved vector is expanded per batch row before top-k)."""
+    words: List[int] = []
+    for meta, n in zip(metas, lengths):
+        w = ALLOW_WORD if resolve(meta) == 1 else DENY_WORD
+        words.extend([w] * int(n))
+    return np.asarray(words, dtype=np.uint32)
+
+
+def decode_word(word: int) -> int:
+    """Device-side decode: exactly one value allows; anything else (malformed) denies."""
+    return 1 if int(word) == ALLOW_WORD else 0
+
+
+def pool(tau: int, n_pub: int, n_priv: int) -> np.ndarray:
+    """Permitted expert ids: the mask m(tau) of Sec. 3.1 is 0 on this set and -inf
+    elsewhere. tau=1 -> private ids [n_pub, n_pub+n_priv); tau=0 -> public [0, n_pub)."""
+    if tau == 1:
+        return np.arange(n_pub, n_pub + n_priv)
+    return np.arange(0, n_pub)
+
+
+# ----------------------------------------------------------------------------
+# Routing (Sec. 3.1 mask equation and the sentence after it; App. B.1)
+# ----------------------------------------------------------------------------
+
+def logits(x_rows: np.ndarray, wr_rows: np.ndarray, bias: Optional[np.ndarray]) -> np.ndarray:
+    """fp32 router logits of the given rows against the given router rows only.
+
+    The dot products are taken in fp64 over the exact input values and rounded once
+    to fp32; a bias is then added with one fp32 addition."""
+    z = (np.asarray(x_rows, np.float64) @ np.asarray(wr_rows, np.float64).T).astype(np.float32)
+    if bias is not None:
+        z = (z + np.asarray(bias, np.float32)[None, :]).astype(np.float32)
+    return z
+
+
+def topk(z: np.ndarray, ids: np.ndarray, k: int):
+    """Top-k of one token's permitted pool.
+
+    Order the pool by (value descending, id ascending) with -0.0 == +0.0 and NaN as
+    -inf; the first k form the selection. Returns (selected ids ascending, gap) where
+    gap = z_(k) - z_(k+1) in fp64, +inf when the pool has exactly k experts."""
+    zz = np.asarray(z, np.float64)
+    zz = np.where(np.isnan(zz), -np.inf, zz) + 0.0
+    order = sorted(range(len(ids)), key=lambda i: (-zz[i], int(ids[i])))
+    sel = [int(ids[i]) for i in order[:k]]
+    if len(ids) == k:
+        gap = np.inf
+    else:
+        a, b = zz[order[k - 1]], zz[order[k]]
+        gap = 0.0 if a == b else float(a - b)
+    return np.asarray(sorted(sel), dtype=np.int64), gap
+
+
+def gates(z_sel: np.ndarray, z_pool: np.ndarray, mode: str) -> np.ndarray:
+    """Gate values in fp64, rounded to fp32. m is the largest selected logit, which is
+    also the pool maximum."""
+    zs = np.asarray(z_sel, np.float64)
+    m = zs.max()
+    num = np.exp(zs - m)
+    if mode == GATE_RENORM:
+        den = num.sum()
+    elif mode == GATE_POOL_SOFTMAX:
+        den = np.exp(np.asarray(z_pool, np.float64) - m).sum()
+    else:
+        raise ValueError(mode)
+    return (num / den).astype(np.float32)
+
+
+@dataclass
+class Route:
+    idx: np.ndarray        # [T, k] int64, ascending per token (global expert ids)
+    gate: np.ndarray       # [T, k] fp32, aligned with idx
+    allow: np.ndarray      # [T] uint8, resolved tau per token
+    gap: np.ndarray        # [T] fp64, k-th minus (k+1)-th masked logit
+    z: List[np.ndarray] = field(default_factory=list)  # per token: fp32 logits of its pool
+
+    @property
+    def near_tie(self) -> np.ndarray:
+        return self.gap < NEAR_TIE
+
+
+def route(x: np.ndarray, wr_pub: np.ndarray, wr_priv: np.ndarray, bias: Optional[np.ndarray],
+          words: Sequence[int], k: int, gate_mode: str = GATE_RENORM) -> Route:
+    """Masked top-k routing of every token. Private router rows are only ever read for
+    tokens whose word allows; an ineligible expert never enters the candidate set."""
+    x = np.asarray(x)
+    T = x.shape[0]
+    n_pub, n_priv = wr_pub.shape[0], wr_priv.shape[0] if wr_priv is not None else 0
+    idx = np.zeros((T, k), np.int64)
+    gate = np.zeros((T, k), np.float32)
+    allow = np.zeros(T, np.uint8)
+    gap = np.zeros(T, np.float64)
+    zs: List[np.ndarray] = [None] * T  # type: ignore
+    taus = np.array([decode_word(w) for w in words], dtype=np.int64)
+    for tau in (0, 1):
+        toks = np.nonzero(taus == tau)[0]
+        if len(toks) == 0:
+            continue
+        ids = pool(tau, n_pub, n_priv)
+        wr = wr_priv if tau == 1 else wr_pub
+        b = None if bias is None else np.asarray(bias, np.float32)[ids]
+        z = logits(x[toks], wr, b)
+        for row, t in enumerate(toks):
+            sel, g = topk(z[row], ids, k)
+            idx[t] = sel
+            gate[t] = gates(z[row][sel - ids[0]], z[row], gate_mode)
+            allow[t] = tau
+            gap[t] = g
+            zs[t] = z[row]
+    return Route(idx, gate, allow, gap, zs)
+
+
+# ----------------------------------------------------------------------------
+# Dispatch: stable grouping of (token, expert) pairs by expert
+# ----------------------------------------------------------------------------
+
+@dataclass
+class Dispatch:
+    count: np.ndarray      # [E] int64
+    offset: np.ndarray     # [E+1] int64, exclusive prefix sum of count
+    row_token: np.ndarray  # [T*k] int64: permuted row -> token
+    token_row: np.ndarray  # [T, k] int64: (token, slot) -> permuted row
+
+
+def dispatch(idx: np.ndarray, n_experts: int) -> Dispatch:
+    """Rows of expert e are the tokens that selected e, in ascending token order;
+    experts follow each other in ascending id order."""
+    T, k = idx.shape
+    count = np.zeros(n_experts, np.int64)
+    offset = np.zeros(n_experts + 1, np.int64)
+    row_token = np.zeros(T * k, np.int64)
+    token_row = np.full((T, k), -1, np.int64)
+    r = 0
+    for e in range(n_experts):
+        offset[e] = r
+        hit = idx == e
+        tokens = np.nonzero(hit.any(axis=1))[0]
+        for t in tokens:
+            j = int(np.nonzero(hit[t])[0][0])
+            row_token[r] = t
+            token_row[t, j] = r
+            r += 1
+        count[e] = len(tokens)
+    offset[n_experts] = r
+    return Dispatch(count, offset, row_token, token_row)
+
+
+# ----------------------------------------------------------------------------
+# Experts
+# ----------------------------------------------------------------------------
+
+def swiglu(X: np.ndarray, w13: np.ndarray, w2: np.ndarray) -> np.ndarray:
+    """One bias-free SwiGLU expert: G = X Wg^T, U = X Wu^T, Y = (silu(G) * U) Wd^T, with
+    w13 = [Wg; Wu] of shape [2I, H] and w2 = Wd of shape [H, I]."""
+    X = np.asarray(X, np.float64)
+    w13 = np.asarray(w13, np.float64)
+    I = w13.shape[0] // 2
+    G = X @ w13[:I].T
+    U = X @ w13[I:].T
+    A = G / (1.0 + np.exp(-G)) * U
+    return A @ np.asarray(w2, np.float64).T
+
+
+class ExecutionHook:
+    """Counts what the private experts physically execute: rows per token and one call
+    per private expert invoked with at least one row (App. F.1 independent hooks)."""
+
+    def __init__(self, n_tokens: int, n_priv: int):
+        self.rows = np.zeros(n_tokens, np.int64)
+        self.calls = np.zeros(n_priv, np.int64)
+
+
+def run_public_expert(X: np.ndarray, w13: np.ndarray, w2: np.ndarray) -> np.ndarray:
+    return swiglu(X, w13, w2)
+
+
+def run_private_expert(p: int, X: np.ndarray, tokens: np.ndarray, w13: np.ndarray,
+                       w2: np.ndarray, hook: ExecutionHook) -> np.ndarray:
+    """Private expert p (0-based within the private pool); the hook records every row."""
+    Y = swiglu(X, w13, w2)
+    for t in tokens:
+        hook.rows[int(t)] += 1
+    if len(tokens) > 0:
+        hook.calls[p] += 1
+    return Y
+
+
+@dataclass
+class LayerResult:
+    route: Route
+    disp: Dispatch
+    out: np.ndarray               # [len(tokens), H] fp64 (rows of the evaluated tokens)
+    tokens: np.ndarray            # evaluated token ids
+    hook: ExecutionHook
+    expert_count: np.ndarray      # [E]
+
+
+def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_priv, w2_priv,
+                  words: Sequence[int], k: int, gate_mode: str = GATE_RENORM,
+                  w13_sh=None, w2_sh=None, tokens: Optional[Sequence[int]] = None) -> LayerResult:
+    """One policy-masked MoE layer. Routing and dispatch cover every token; expert
+    outputs are evaluated for `tokens` (all by default). Weight containers are
+    indexed by expert (e.g. w13_pub[e] -> [2I, H])."""
+    x = np.asarray(x)
+    T = x.shape[0]
+    n_pub = wr_pub.shape[0]
+    n_priv = wr_priv.shape[0] if wr_priv is not None else 0
+    E = n_pub + n_priv
+    rt = route(x, wr_pub, wr_priv, bias, words, k, gate_mode)
+    dp = dispatch(rt.idx, E)
+    toks = np.arange(T) if tokens is None else np.asarray(tokens, np.int64)
+    hook = ExecutionHook(T, n_priv)
+    y: Dict[tuple, np.ndarray] = {}
+    for e in range(E):
+        rows = np.asarray([t for t in toks if e in rt.idx[t]], np.int64)
+        if len(rows) == 0:
+            continue
+        X = x[rows]
+        if e < n_pub:
+            Y = run_public_expert(X, w13_pub[e], w2_pub[e])
+        else:
+            Y = run_private_expert(e - n_pub, X, rows, w13_priv[e - n_pub], w2_priv[e - n_pub], hook)
+        for i, t in enumerate(rows):
+            y[(int(t), e)] = Y[i]
+    H = x.shape[1]
+    out = np.zeros((len(toks), H), np.float64)
+    ysh = swiglu(x[toks], w13_sh, w2_sh) if w13_sh is not None else None
+    for i, t in enumerate(toks):
+        acc = np.zeros(H, np.float64)
+        for j in range(k):
+            acc += np.float64(rt.gate[t, j]) * y[(int(t), int(rt.idx[t, j]))]
+        if ysh is not None:
+            acc += ysh[i]
+        out[i] = acc
+    return LayerResult(rt, dp, out, toks, hook, dp.count)
+
+
+# ----------------------------------------------------------------------------
+# Audit (App. B.2 row-indexed route counters; App. F.1)
+# ----------------------------------------------------------------------------
+
+def route_private_rows(idx: np.ndarray, n_pub: int) -> np.ndarray:
+    """Route-log count per token: how many of its selected experts are private."""
+    return (np.asarray(idx) >= n_pub).sum(axis=1).astype(np.int64)
+
+
+@dataclass
+class Audit:
+    req_private_rows: np.ndarray   # [R] int64
+    total_private_rows: int
+    deny_violations: int           # tokens with allow == 0 and a nonzero private-row count
+
+
+def audit(token_rows: np.ndarray, allow: np.ndarray, req_offset: Sequence[int]) -> Audit:
+    token_rows = np.asarray(token_rows, np.int64)
+    R = len(req_offset) - 1
+    req = np.zeros(R, np.int64)
+    for r in range(R):
+        req[r] = int(token_rows[req_offset[r]:req_offset[r + 1]].sum())
+    viol = int(((np.asarray(allow) == 0) & (token_rows > 0)).sum())
+    return Audit(req, int(req.sum()), viol)
