@@ -1,0 +1,244 @@
+/*
+ * pmpe.h - C ABI of libpmpe, the forward pass of one policy-masked MoE layer on an
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: Policy-Masked Private Experts (arXiv 2608.06690). Trusted per-request
+ * authorization tau selects either the original public expert pool or a disjoint,
+ * added private pool; the hard mask m(tau) is applied to the router logits BEFORE
+ * top-k (Sec. 3.1, mask equation), so an ineligible expert never enters the
+ * candidate set (App. B.1). Missing or malformed authorization resolves to deny
+ * (Sec. 3.1 resolver paragraph; App. B.1). A separate execution audit counts the
+ * private rows that were physically executed (App. F.1, independent hooks; App. B.2,
+ * row-indexed route counters).
+ *
+ * One layer forward is five calls, all asynchronous on one HIP stream:
+ *
+ *   pmpe_route       policy decode, masked fp32 router logits, top-k, gates
+ *   pmpe_dispatch    per-expert counts, offsets, stable permutation, row gather
+ *   pmpe_expert_ffn  SwiGLU experts (grouped GEMM) + private-row execution audit
+ *   pmpe_combine     out[t] = sum_j gate[t,j] * y[t, expert j] (+ shared experts)
+ *   pmpe_audit       per-request private rows, total, deny violations
+ *
+ * Conventions for every call
+ * - All pointers except `d` are DEVICE pointers unless stated otherwise; `d` (the
+ *   layer descriptor) is a host pointer read during the call only.
+ * - The caller owns and allocates every buffer, including the workspace. The library
+ *   allocates nothing and keeps no pointer after a call returns.
+ * - Host-side validation runs before any launch; on failure the call returns a
+ *   negative pmpe_status, launches nothing and writes nothing. Errors inside kernels
+ *   surface at the caller's next synchronisation; conditions only the device can
+ *   see (e.g. private rows reaching a NULL private weight pointer) set bits in the
+ *   optional `dev_status` word.
+ * - Calls are stream-ordered; a workspace may be shared by calls on one stream.
+ * - T = 0 is valid: nothing is launched and PMPE_OK is returned.
+ * - Row-major layouts throughout. Expert ids: public [0, n_pub), private
+ *   [n_pub, n_pub + n_priv).
+ * - No C++ exception crosses this ABI.
+ */
+#ifndef PMPE_H
+#define PMPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Opaque HIP stream handle (identical to hipStream_t); NULL = the default stream. */
+typedef struct ihipStream_t* pmpe_stream_t;
+
+typedef enum {
+  PMPE_OK = 0,
+  PMPE_ERR_NULL = -1,            /* a required pointer is NULL */
+  PMPE_ERR_SHAPE = -2,           /* a size is out of the supported range */
+  PMPE_ERR_K_EXCEEDS_POOL = -3,  /* top_k > n_pub or top_k > n_priv */
+  PMPE_ERR_DTYPE = -4,           /* unsupported dtype combination */
+  PMPE_ERR_ALIGN = -5,           /* a pointer is not 16-byte aligned */
+  PMPE_ERR_WORKSPACE = -6,       /* workspace missing or smaller than pmpe_workspace_bytes */
+  PMPE_ERR_LAUNCH = -7           /* the HIP runtime refused a launch */
+} pmpe_status;
+
+typedef enum { PMPE_F32 = 0, PMPE_BF16 = 1 } pmpe_dtype;
+
+/* Gate normalisation (the paper does not fix it):
+ * RENORM        softmax over the k selected logits (= pool softmax renormalised over
+ *               the top-k);
+ * POOL_SOFTMAX  softmax over the whole permitted pool, gates not renormalised. */
+typedef enum { PMPE_GATE_RENORM_TOPK = 0, PMPE_GATE_POOL_SOFTMAX = 1 } pmpe_gate_mode;
+
+/* Policy words. Exactly one 32-bit value allows; every other value - including
+ * corrupted words - is malformed and resolves to deny (fail closed). */
+#define PMPE_POLICY_ALLOW 0xA11C0DE5u
+#define PMPE_POLICY_DENY 0x00000000u
+
+/* Bits of the optional device status word. */
+#define PMPE_DEV_PRIV_ROUTER_MISSING 0x1u  /* allow rows met wr_priv == NULL: routed as deny */
+#define PMPE_DEV_PRIV_WEIGHTS_MISSING 0x2u /* private rows met NULL private expert weights:
+                                              those rows were NOT executed, outputs zeroed */
+
+/* Supported ranges (checked by host validation). */
+#define PMPE_MAX_POOL 256  /* n_pub and n_priv each in [top_k, 256] */
+#define PMPE_MAX_TOPK 16
+#define PMPE_MAX_TOKENS (1 << 24)
+
+typedef struct {
+  int32_t hidden;       /* H, multiple of 64, <= 16384 */
+  int32_t inter;        /* I of one routed expert, multiple of 64 */
+  int32_t n_pub;        /* public (original, frozen) experts */
+  int32_t n_priv;       /* private (added) experts */
+  int32_t top_k;        /* k, 1..16, k <= min(n_pub, n_priv) */
+  int32_t n_shared;     /* always-on shared experts (0 = none) */
+  int32_t shared_inter; /* I of one shared expert (multiple of 64 when n_shared > 0) */
+  int32_t act_dtype;    /* pmpe_dtype of x, x_perm, y_perm, y_shared, out */
+  int32_t w_dtype;      /* pmpe_dtype of expert weights; must equal act_dtype */
+  int32_t gate_mode;    /* pmpe_gate_mode */
+} pmpe_layer_desc;
+
+/* Bytes of workspace that any call below may need for T tokens (the maximum over
+ * the calls, so one buffer serves all of them). 0 if the descriptor is invalid. */
+size_t pmpe_workspace_bytes(const pmpe_layer_desc* d, int32_t T);
+
+/* Static, NUL-terminated description of a pmpe_status value. */
+const char* pmpe_status_string(int32_t status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t pmpe_version(void);
+
+/* Validation only: returns what pmpe_route would return for these arguments, without
+ * launching. Lets a host without a GPU check arguments. */
+pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T);
+
+/*
+ * pmpe_route - policy decode, masked router logits, top-k and gates.
+ * (Sec. 3.1 mask equation and the sentence after it; App. B.1 masked routing and
+ * steps 2 and 4 of the fail-closed request procedure.)
+ *
+ * For token t: tau_t = (policy_word[t] == PMPE_POLICY_ALLOW). The permitted pool is
+ * the private ids if tau_t, else the public ids. Logits z_e = fp32(x_t . W_r[e]) (+
+ * logit_bias[e], one fp32 add) are computed for the permitted pool ONLY: the other
+ * pool's logits are never formed, and a deny token's x is never multiplied with
+ * private router rows. The k largest logits win, equal fp32 values going to the
+ * lower expert id (-0.0 == +0.0).
+ *
+ *   x            [T, H] act_dtype
+ *   wr_pub       [n_pub, H] fp32, frozen router rows
+ *   wr_priv      [n_priv, H] fp32, private gate rows; never read unless some token
+ *                allows; may be NULL (allow tokens then route as deny and
+ *                PMPE_DEV_PRIV_ROUTER_MISSING is set)
+ *   logit_bias   [n_pub + n_priv] fp32 or NULL
+ *   policy_word  [T] uint32 or NULL (NULL: every token denies)
+ *   topk_idx     [T, k] int32 out: global expert ids, ascending within a token
+ *   topk_gate    [T, k] fp32 out, aligned with topk_idx
+ *   allow        [T] uint8 out: resolved tau (the route log's policy decision)
+ *   kgap         [T] fp32 out or NULL: k-th minus (k+1)-th largest masked logit,
+ *                +inf when the pool has exactly k experts
+ *   dev_status   [1] uint32 in/out or NULL: status bits are OR-ed in
+ */
+pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const float* wr_pub,
+                       const float* wr_priv, const float* logit_bias, const uint32_t* policy_word,
+                       int32_t* topk_idx, float* topk_gate, uint8_t* allow, float* kgap,
+                       uint32_t* dev_status, pmpe_stream_t stream);
+
+/*
+ * pmpe_dispatch - group the T*k (token, expert) pairs by expert.
+ * (Token permutation of the MoE forward; no passage of the paper describes it.)
+ *
+ * Rows of expert e are the tokens that selected e, in ascending token order; experts
+ * are laid out in ascending id order. Deterministic (no order-dependent atomics).
+ *
+ *   topk_idx       [T, k] int32 from pmpe_route
+ *   x              [T, H] act_dtype (read only if x_perm != NULL)
+ *   expert_count   [E] int32 out, E = n_pub + n_priv
+ *   expert_offset  [E + 1] int32 out: exclusive prefix sum of expert_count
+ *   row_token      [T*k] int32 out: permuted row -> token
+ *   token_row      [T*k] int32 out: (t, j) -> permuted row of token t's j-th expert
+ *   x_perm         [T*k, H] act_dtype out or NULL: x gathered in permuted order; with
+ *                  NULL, pmpe_expert_ffn gathers rows from x itself
+ *   ws, ws_bytes   workspace, at least pmpe_workspace_bytes(d, T)
+ */
+pmpe_status pmpe_dispatch(const pmpe_layer_desc* d, int32_t T, const int32_t* topk_idx,
+                          const void* x, int32_t* expert_count, int32_t* expert_offset,
+                          int32_t* row_token, int32_t* token_row, void* x_perm, void* ws,
+                          size_t ws_bytes, pmpe_stream_t stream);
+
+/*
+ * pmpe_expert_ffn - run every expert with at least one row, and the shared group.
+ * (Disjoint private pool copying the expert architecture, Sec. 3.1; bias-free SwiGLU
+ * with gate, up and down projections, Sec. 4.2; execution audit, App. F.1.)
+ *
+ * For expert e with n_e = expert_count[e] > 0 rows X (rows offset_e .. offset_e+n_e-1
+ * of x_perm, or x[row_token[r]] when x_perm is NULL):
+ *   h = silu(X Wg^T) * (X Wu^T)   (fp32 accumulate, h rounded to act_dtype)
+ *   y_perm[rows] = h Wd^T         (fp32 accumulate, rounded to act_dtype)
+ * Experts with zero rows load no weights and write nothing. Private weights are read
+ * only for private experts that have rows, so an all-deny batch works with every
+ * private pointer NULL.
+ *
+ * Audit (written here, by the code that executes the rows, not from the route log):
+ *   audit_token_rows[row_token[r]] += 1 for every executed private row r;
+ *   audit_priv_calls[e - n_pub]     += 1 for every private expert run with >= 1 row.
+ * Both accumulate across calls; the caller zeroes them between decisions.
+ *
+ *   w13_pub   [n_pub, 2I, H]: rows [0, I) gate projection, rows [I, 2I) up projection
+ *   w2_pub    [n_pub, H, I]: down projection
+ *   w13_priv  [n_priv, 2I, H], w2_priv [n_priv, H, I]; may be NULL when no private row
+ *             exists (otherwise PMPE_DEV_PRIV_WEIGHTS_MISSING is set, the rows are not
+ *             executed, not audited, and their y_perm rows are zero)
+ *   x         [T, H] act_dtype: needed if x_perm == NULL or n_shared > 0
+ *   w13_sh    [2 Is, H], w2_sh [H, Is], Is = n_shared * shared_inter: the shared
+ *             experts as one SwiGLU whose intermediate is their concatenation
+ *             (gate rows of all shared experts, then their up rows); NULL if
+ *             n_shared == 0
+ *   y_shared  [T, H] act_dtype out (shared-group output), NULL if n_shared == 0
+ *   y_perm    [T*k, H] act_dtype out
+ *   audit_token_rows [T] uint32 in/out;  audit_priv_calls [n_priv] uint32 in/out or NULL
+ *   dev_status [1] uint32 in/out or NULL
+ */
+pmpe_status pmpe_expert_ffn(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                            const void* x, const int32_t* expert_count,
+                            const int32_t* expert_offset, const int32_t* row_token,
+                            const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                            const void* w2_priv, const void* w13_sh, const void* w2_sh,
+                            void* y_shared, void* y_perm, uint32_t* audit_token_rows,
+                            uint32_t* audit_priv_calls, uint32_t* dev_status, void* ws,
+                            size_t ws_bytes, pmpe_stream_t stream);
+
+/*
+ * pmpe_combine - merge the selected experts' outputs into the layer output.
+ * (Merge into the frozen upper transformer, Fig. 1 and Sec. 3.1.)
+ *
+ *   out[t] = sum_{j<k} topk_gate[t,j] * y_perm[token_row[t,j]]  (+ y_shared[t])
+ * accumulated in fp32 in slot order j = 0..k-1 and rounded once to act_dtype, so
+ * the result is bitwise deterministic.
+ *
+ *   y_perm [T*k, H], token_row [T*k], topk_gate [T*k] fp32, y_shared [T, H] or NULL,
+ *   out [T, H] act_dtype
+ */
+pmpe_status pmpe_combine(const pmpe_layer_desc* d, int32_t T, const void* y_perm,
+                         const int32_t* token_row, const float* topk_gate,
+                         const void* y_shared, void* out, pmpe_stream_t stream);
+
+/*
+ * pmpe_audit - reduce the execution audit per request.
+ * (Route counters indexed by row, App. B.2; zero private execution under deny, G1.)
+ *
+ *   audit_token_rows   [T] uint32 from pmpe_expert_ffn
+ *   allow              [T] uint8 from pmpe_route
+ *   req_offset         [R + 1] int32: request r owns tokens [req_offset[r],
+ *                      req_offset[r+1]); non-decreasing, req_offset[0] = 0,
+ *                      req_offset[R] = T (a device array)
+ *   req_private_rows   [R] uint64 out
+ *   total_private_rows [1] uint64 out
+ *   deny_violations    [1] uint32 out: tokens with allow == 0 and a nonzero count
+ */
+pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audit_token_rows,
+                       const uint8_t* allow, const int32_t* req_offset, int32_t R,
+                       uint64_t* req_private_rows, uint64_t* total_private_rows,
+                       uint32_t* deny_violations, pmpe_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PMPE_H */

@@ -1,0 +1,10 @@
+"""MI355X-native policy-masked MoE layer (Policy-Masked Private Experts, arXiv 2608.06690).
+
+The computation lives in libpmpe.so (HIP kernels for gfx950 behind the C ABI of
+include/pmpe.h); this package is its binding."""
+from ._native import (PMPE_BF16, PMPE_F32, PMPE_GATE_POOL_SOFTMAX, PMPE_GATE_RENORM_TOPK,  # noqa: F401
+                      PMPE_POLICY_ALLOW, PMPE_POLICY_DENY, LayerDesc, PmpeError, make_desc,
+                      pmpe_audit, pmpe_check_desc, pmpe_combine, pmpe_dispatch, pmpe_expert_ffn,
+                      pmpe_route, pmpe_version, pmpe_workspace_bytes)
+from .layer import AuditBuffers, LayerBuffers, PolicyMaskedMoE  # noqa: F401
+from .policy import policy_word, request_offsets, resolve_policy, token_policy_words  # noqa: F401

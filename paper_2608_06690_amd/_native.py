@@ -1,0 +1,160 @@
+"""ctypes binding of libpmpe (include/pmpe.h): argument marshalling only.
+
+Every function has the name of the C entry point and takes torch tensors (or None)
+where the C call takes device pointers; the HIP stream defaults to torch's current
+stream. A negative status raises PmpeError. Every step of the layer runs in the HIP
+kernels of libpmpe; if the library is missing, importing this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpmpe.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is not built; run `python -m paper_2608_06690_amd.build` "
+        "(or __graft_entry__.build()) first")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+PMPE_OK = 0
+PMPE_F32 = 0
+PMPE_BF16 = 1
+PMPE_GATE_RENORM_TOPK = 0
+PMPE_GATE_POOL_SOFTMAX = 1
+PMPE_POLICY_ALLOW = 0xA11C0DE5
+PMPE_POLICY_DENY = 0x00000000
+PMPE_DEV_PRIV_ROUTER_MISSING = 0x1
+PMPE_DEV_PRIV_WEIGHTS_MISSING = 0x2
+
+STATUS_NAMES = {
+    0: "PMPE_OK", -1: "PMPE_ERR_NULL", -2: "PMPE_ERR_SHAPE", -3: "PMPE_ERR_K_EXCEEDS_POOL",
+    -4: "PMPE_ERR_DTYPE", -5: "PMPE_ERR_ALIGN", -6: "PMPE_ERR_WORKSPACE", -7: "PMPE_ERR_LAUNCH",
+}
+
+
+class PmpeError(RuntimeError):
+    def __init__(self, status: int, call: str):
+        self.status = status
+        msg = _lib.pmpe_status_string(status).decode()
+        super().__init__(f"{call}: {STATUS_NAMES.get(status, status)} ({msg})")
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "hidden", "inter", "n_pub", "n_priv", "top_k", "n_shared", "shared_inter",
+        "act_dtype", "w_dtype", "gate_mode")]
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+_DESC = ctypes.POINTER(LayerDesc)
+
+_lib.pmpe_version.restype = _I32
+_lib.pmpe_version.argtypes = []
+_lib.pmpe_status_string.restype = ctypes.c_char_p
+_lib.pmpe_status_string.argtypes = [_I32]
+_lib.pmpe_workspace_bytes.restype = _SZ
+_lib.pmpe_workspace_bytes.argtypes = [_DESC, _I32]
+_lib.pmpe_check_desc.restype = _I32
+_lib.pmpe_check_desc.argtypes = [_DESC, _I32]
+_lib.pmpe_route.restype = _I32
+_lib.pmpe_route.argtypes = [_DESC, _I32] + [_P] * 10 + [_P]
+_lib.pmpe_dispatch.restype = _I32
+_lib.pmpe_dispatch.argtypes = [_DESC, _I32] + [_P] * 7 + [_P, _SZ, _P]
+_lib.pmpe_expert_ffn.restype = _I32
+_lib.pmpe_expert_ffn.argtypes = [_DESC, _I32] + [_P] * 16 + [_P, _SZ, _P]
+_lib.pmpe_combine.restype = _I32
+_lib.pmpe_combine.argtypes = [_DESC, _I32] + [_P] * 5 + [_P]
+_lib.pmpe_audit.restype = _I32
+_lib.pmpe_audit.argtypes = [_DESC, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]
+
+EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_check_desc",
+            "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit"]
+
+
+def lib() -> ctypes.CDLL:
+    return _lib
+
+
+def make_desc(hidden: int, inter: int, n_pub: int, n_priv: int, top_k: int, n_shared: int = 0,
+              shared_inter: int = 0, bf16: bool = True, gate_mode: int = PMPE_GATE_RENORM_TOPK
+              ) -> LayerDesc:
+    dt = PMPE_BF16 if bf16 else PMPE_F32
+    return LayerDesc(hidden, inter, n_pub, n_priv, top_k, n_shared, shared_inter, dt, dt, gate_mode)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libpmpe must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _check(status: int, call: str) -> None:
+    if status != PMPE_OK:
+        raise PmpeError(status, call)
+
+
+def pmpe_version() -> int:
+    return int(_lib.pmpe_version())
+
+
+def pmpe_workspace_bytes(desc: LayerDesc, T: int) -> int:
+    return int(_lib.pmpe_workspace_bytes(ctypes.byref(desc), T))
+
+
+def pmpe_check_desc(desc: LayerDesc, T: int) -> int:
+    return int(_lib.pmpe_check_desc(ctypes.byref(desc), T))
+
+
+def pmpe_route(desc, T, x, wr_pub, wr_priv, logit_bias, policy_word, topk_idx, topk_gate, allow,
+               kgap=None, dev_status=None, stream=None) -> None:
+    _check(_lib.pmpe_route(ctypes.byref(desc), T, _ptr(x), _ptr(wr_pub), _ptr(wr_priv),
+                           _ptr(logit_bias), _ptr(policy_word), _ptr(topk_idx), _ptr(topk_gate),
+                           _ptr(allow), _ptr(kgap), _ptr(dev_status), _stream(stream)), "pmpe_route")
+
+
+def pmpe_dispatch(desc, T, topk_idx, x, expert_count, expert_offset, row_token, token_row, x_perm,
+                  ws, stream=None) -> None:
+    _check(_lib.pmpe_dispatch(ctypes.byref(desc), T, _ptr(topk_idx), _ptr(x), _ptr(expert_count),
+                              _ptr(expert_offset), _ptr(row_token), _ptr(token_row), _ptr(x_perm),
+                              _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                              _stream(stream)), "pmpe_dispatch")
+
+
+def pmpe_expert_ffn(desc, T, x_perm, x, expert_count, expert_offset, row_token, w13_pub, w2_pub,
+                    w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm, audit_token_rows,
+                    audit_priv_calls, dev_status, ws, stream=None) -> None:
+    _check(_lib.pmpe_expert_ffn(
+        ctypes.byref(desc), T, _ptr(x_perm), _ptr(x), _ptr(expert_count), _ptr(expert_offset),
+        _ptr(row_token), _ptr(w13_pub), _ptr(w2_pub), _ptr(w13_priv), _ptr(w2_priv), _ptr(w13_sh),
+        _ptr(w2_sh), _ptr(y_shared), _ptr(y_perm), _ptr(audit_token_rows), _ptr(audit_priv_calls),
+        _ptr(dev_status), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)), "pmpe_expert_ffn")
+
+
+def pmpe_combine(desc, T, y_perm, token_row, topk_gate, y_shared, out, stream=None) -> None:
+    _check(_lib.pmpe_combine(ctypes.byref(desc), T, _ptr(y_perm), _ptr(token_row), _ptr(topk_gate),
+                             _ptr(y_shared), _ptr(out), _stream(stream)), "pmpe_combine")
+
+
+def pmpe_audit(desc, T, audit_token_rows, allow, req_offset, R, req_private_rows,
+               total_private_rows, deny_violations, stream=None) -> None:
+    _check(_lib.pmpe_audit(ctypes.byref(desc), T, _ptr(audit_token_rows), _ptr(allow),
+                           _ptr(req_offset), R, _ptr(req_private_rows), _ptr(total_private_rows),
+                           _ptr(deny_violations), _stream(stream)), "pmpe_audit")

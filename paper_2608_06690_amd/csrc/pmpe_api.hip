@@ -1,0 +1,178 @@
+// C ABI of libpmpe: argument validation (host only, before any launch) and dispatch to
+// the kernel launchers. No exception crosses this boundary; nothing is allocated.
+#include <new>
+
+#include "pmpe_internal.h"
+
+using namespace pmpe;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+size_t elem_bytes(const pmpe_layer_desc* d) { return d->act_dtype == PMPE_BF16 ? 2 : 4; }
+
+pmpe_status check_desc(const pmpe_layer_desc* d, int32_t T) {
+  if (d == nullptr) return PMPE_ERR_NULL;
+  if (T < 0 || T > PMPE_MAX_TOKENS) return PMPE_ERR_SHAPE;
+  if (d->act_dtype != PMPE_F32 && d->act_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
+  if (d->w_dtype != d->act_dtype) return PMPE_ERR_DTYPE;
+  if (d->hidden < 128 || d->hidden > 16384 || d->hidden % 128 != 0) return PMPE_ERR_SHAPE;
+  if (d->inter < 64 || d->inter > 65536 || d->inter % 64 != 0) return PMPE_ERR_SHAPE;
+  if (d->top_k < 1 || d->top_k > PMPE_MAX_TOPK) return PMPE_ERR_SHAPE;
+  if (d->n_pub < 1 || d->n_pub > PMPE_MAX_POOL || d->n_priv < 0 || d->n_priv > PMPE_MAX_POOL)
+    return PMPE_ERR_SHAPE;
+  if (d->top_k > d->n_pub || d->top_k > d->n_priv) return PMPE_ERR_K_EXCEEDS_POOL;
+  if (d->n_shared < 0 || d->n_shared > 64) return PMPE_ERR_SHAPE;
+  if (d->n_shared > 0) {
+    if (d->shared_inter < 64 || d->shared_inter % 64 != 0) return PMPE_ERR_SHAPE;
+    if ((int64_t)d->n_shared * d->shared_inter > 65536) return PMPE_ERR_SHAPE;
+  }
+  if (d->gate_mode != PMPE_GATE_RENORM_TOPK && d->gate_mode != PMPE_GATE_POOL_SOFTMAX)
+    return PMPE_ERR_SHAPE;
+  if ((int64_t)T * d->top_k > (int64_t)INT32_MAX / 2) return PMPE_ERR_SHAPE;
+  return PMPE_OK;
+}
+
+size_t dispatch_ws(const pmpe_layer_desc* d, int32_t T) {
+  const size_t E = (size_t)d->n_pub + d->n_priv;
+  return round_up((size_t)dispatch_chunks(T) * E * 4) + round_up((size_t)T * d->top_k * 4);
+}
+
+size_t ffn_ws(const pmpe_layer_desc* d, int32_t T) {
+  const size_t el = elem_bytes(d);
+  const size_t Is = (size_t)d->n_shared * d->shared_inter;
+  return round_up((size_t)T * d->top_k * d->inter * el) + round_up((size_t)T * Is * el);
+}
+
+pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t pmpe_version(void) { return 10000; }
+
+const char* pmpe_status_string(int32_t status) {
+  switch (status) {
+    case PMPE_OK: return "ok";
+    case PMPE_ERR_NULL: return "a required pointer is NULL";
+    case PMPE_ERR_SHAPE: return "a size is out of the supported range";
+    case PMPE_ERR_K_EXCEEDS_POOL: return "top_k exceeds the public or the private pool";
+    case PMPE_ERR_DTYPE: return "unsupported dtype combination";
+    case PMPE_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+    case PMPE_ERR_WORKSPACE: return "workspace missing or too small";
+    case PMPE_ERR_LAUNCH: return "the HIP runtime refused a kernel launch";
+    default: return "unknown status";
+  }
+}
+
+pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T) { return check_desc(d, T); }
+
+size_t pmpe_workspace_bytes(const pmpe_layer_desc* d, int32_t T) {
+  if (check_desc(d, T) != PMPE_OK) return 0;
+  const size_t a = dispatch_ws(d, T), b = ffn_ws(d, T);
+  return a > b ? a : b;
+}
+
+pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const float* wr_pub,
+                       const float* wr_priv, const float* logit_bias, const uint32_t* policy_word,
+                       int32_t* topk_idx, float* topk_gate, uint8_t* allow, float* kgap,
+                       uint32_t* dev_status, pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (!x || !wr_pub || !topk_idx || !topk_gate || !allow) return PMPE_ERR_NULL;
+  if (!aligned16(x) || !aligned16(wr_pub) || (wr_priv && !aligned16(wr_priv))) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  RouteArgs a{T, d->hidden, d->n_pub, d->n_priv, d->top_k, d->gate_mode,
+              d->act_dtype == PMPE_BF16, x, wr_pub, wr_priv, logit_bias, policy_word,
+              topk_idx, topk_gate, allow, kgap, dev_status};
+  return launched(launch_route(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_dispatch(const pmpe_layer_desc* d, int32_t T, const int32_t* topk_idx,
+                          const void* x, int32_t* expert_count, int32_t* expert_offset,
+                          int32_t* row_token, int32_t* token_row, void* x_perm, void* ws,
+                          size_t ws_bytes, pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (!topk_idx || !expert_count || !expert_offset || !row_token || !token_row) return PMPE_ERR_NULL;
+  if (x_perm && !x) return PMPE_ERR_NULL;
+  if (x_perm && (!aligned16(x) || !aligned16(x_perm))) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  if (!ws || ws_bytes < dispatch_ws(d, T)) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  const int E = d->n_pub + d->n_priv;
+  int32_t* chunk_base = (int32_t*)ws;
+  int32_t* rank = (int32_t*)((char*)ws + round_up((size_t)dispatch_chunks(T) * E * 4));
+  DispatchArgs a{T, d->top_k, E, d->hidden, d->act_dtype == PMPE_BF16, topk_idx, x,
+                 expert_count, expert_offset, row_token, token_row, x_perm, chunk_base, rank};
+  return launched(launch_dispatch(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_expert_ffn(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                            const void* x, const int32_t* expert_count,
+                            const int32_t* expert_offset, const int32_t* row_token,
+                            const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                            const void* w2_priv, const void* w13_sh, const void* w2_sh,
+                            void* y_shared, void* y_perm, uint32_t* audit_token_rows,
+                            uint32_t* audit_priv_calls, uint32_t* dev_status, void* ws,
+                            size_t ws_bytes, pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (!expert_count || !expert_offset || !row_token || !w13_pub || !w2_pub || !y_perm ||
+      !audit_token_rows)
+    return PMPE_ERR_NULL;
+  if (!x_perm && !x) return PMPE_ERR_NULL;
+  if (d->n_shared > 0 && (!x || !w13_sh || !w2_sh || !y_shared)) return PMPE_ERR_NULL;
+  const void* al[] = {x_perm, x, w13_pub, w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  if (!ws || ws_bytes < ffn_ws(d, T)) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  const size_t el = elem_bytes(d);
+  const int Is = d->n_shared * d->shared_inter;
+  void* h = ws;
+  void* h_sh = (char*)ws + round_up((size_t)T * d->top_k * d->inter * el);
+  FfnArgs a{T, d->hidden, d->inter, d->n_pub, d->n_priv, d->top_k, d->act_dtype == PMPE_BF16,
+            d->n_shared > 0 ? Is : 0, x_perm, x, expert_count, expert_offset, row_token,
+            w13_pub, w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm,
+            audit_token_rows, audit_priv_calls, dev_status, h, h_sh};
+  return launched(launch_expert_ffn(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_combine(const pmpe_layer_desc* d, int32_t T, const void* y_perm,
+                         const int32_t* token_row, const float* topk_gate,
+                         const void* y_shared, void* out, pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (!y_perm || !token_row || !topk_gate || !out) return PMPE_ERR_NULL;
+  if (d->n_shared > 0 && !y_shared) return PMPE_ERR_NULL;
+  if (!aligned16(y_perm) || !aligned16(out) || (y_shared && !aligned16(y_shared))) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  CombineArgs a{T, d->hidden, d->top_k, d->act_dtype == PMPE_BF16, y_perm, token_row,
+                topk_gate, d->n_shared > 0 ? y_shared : nullptr, out};
+  return launched(launch_combine(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audit_token_rows,
+                       const uint8_t* allow, const int32_t* req_offset, int32_t R,
+                       uint64_t* req_private_rows, uint64_t* total_private_rows,
+                       uint32_t* deny_violations, pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (R < 0 || R > PMPE_MAX_TOKENS) return PMPE_ERR_SHAPE;
+  if (!total_private_rows || !deny_violations) return PMPE_ERR_NULL;
+  if (T > 0 && (!audit_token_rows || !allow)) return PMPE_ERR_NULL;
+  if (R > 0 && (!req_offset || !req_private_rows)) return PMPE_ERR_NULL;
+  AuditArgs a{T, R, audit_token_rows, allow, req_offset, req_private_rows, total_private_rows,
+              deny_violations};
+  return launched(launch_audit(a, (hipStream_t)stream));
+}
+
+}  // extern "C"

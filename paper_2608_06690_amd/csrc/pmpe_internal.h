@@ -1,0 +1,152 @@
+// Internal declarations of libpmpe: device helpers and the launchers that the C ABI
+// (pmpe_api.hip) calls after validating its arguments. gfx950 (CDNA4) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "pmpe.h"
+
+namespace pmpe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// bf16 helpers (raw uint16 storage; conversions exact or round-to-nearest-even)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;  // quiet NaN
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+// Two floats -> packed bf16 pair (low half = a).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return f32_to_bf16_rne(a) | (f32_to_bf16_rne(b) << 16);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+
+// Wave-level helpers (wave64).
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+  // butterfly: every lane ends with the bitwise-identical total
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int o = __shfl_up(v, off, 64);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  lo = __shfl_xor(lo, mask, 64);
+  hi = __shfl_xor(hi, mask, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  lo = __shfl(lo, src, 64);
+  hi = __shfl(hi, src, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (arguments already validated; T > 0)
+// ---------------------------------------------------------------------------
+struct RouteArgs {
+  int T, H, n_pub, n_priv, k, gate_mode, act_bf16;
+  const void* x;
+  const float* wr_pub;
+  const float* wr_priv;
+  const float* bias;
+  const uint32_t* words;
+  int32_t* topk_idx;
+  float* topk_gate;
+  uint8_t* allow;
+  float* kgap;
+  uint32_t* dev_status;
+};
+hipError_t launch_route(const RouteArgs& a, hipStream_t s);
+
+struct DispatchArgs {
+  int T, k, E, H, act_bf16;
+  const int32_t* topk_idx;
+  const void* x;
+  int32_t* count;
+  int32_t* offset;
+  int32_t* row_token;
+  int32_t* token_row;
+  void* x_perm;
+  int32_t* chunk_base;  // workspace [nchunks, E]
+  int32_t* rank;        // workspace [T*k]
+};
+int dispatch_chunks(int T);
+hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s);
+
+struct FfnArgs {
+  int T, H, I, n_pub, n_priv, k, act_bf16;
+  int Is;  // shared intermediate (0 = no shared group)
+  const void* x_perm;
+  const void* x;
+  const int32_t* count;
+  const int32_t* offset;
+  const int32_t* row_token;
+  const void* w13_pub;
+  const void* w2_pub;
+  const void* w13_priv;
+  const void* w2_priv;
+  const void* w13_sh;
+  const void* w2_sh;
+  void* y_shared;
+  void* y_perm;
+  uint32_t* audit_rows;
+  uint32_t* audit_calls;
+  uint32_t* dev_status;
+  void* h;     // workspace [T*k, I]
+  void* h_sh;  // workspace [T, Is]
+};
+hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
+
+struct CombineArgs {
+  int T, H, k, act_bf16;
+  const void* y_perm;
+  const int32_t* token_row;
+  const float* gate;
+  const void* y_shared;
+  void* out;
+};
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+
+struct AuditArgs {
+  int T, R;
+  const uint32_t* rows;
+  const uint8_t* allow;
+  const int32_t* req_offset;
+  uint64_t* req_rows;
+  uint64_t* total;
+  uint32_t* violations;
+};
+hipError_t launch_audit(const AuditArgs& a, hipStream_t s);
+
+}  // namespace pmpe

@@ -1,0 +1,137 @@
+"""PolicyMaskedMoE: owns one layer's device buffers and runs the five C-ABI calls in
+order on one stream (route -> dispatch -> expert_ffn -> combine -> audit). It only
+allocates torch tensors and passes pointers; all computation happens in libpmpe."""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import torch
+
+from . import _native as N
+
+
+@dataclasses.dataclass
+class LayerBuffers:
+    topk_idx: torch.Tensor
+    topk_gate: torch.Tensor
+    allow: torch.Tensor
+    kgap: torch.Tensor
+    expert_count: torch.Tensor
+    expert_offset: torch.Tensor
+    row_token: torch.Tensor
+    token_row: torch.Tensor
+    x_perm: Optional[torch.Tensor]
+    y_perm: torch.Tensor
+    y_shared: Optional[torch.Tensor]
+    out: torch.Tensor
+    ws: torch.Tensor
+    dev_status: torch.Tensor
+
+
+@dataclasses.dataclass
+class AuditBuffers:
+    token_rows: torch.Tensor    # [T] uint32 (int32 storage), accumulates across calls
+    priv_calls: torch.Tensor    # [n_priv]
+    req_rows: torch.Tensor      # [R] uint64 (int64 storage)
+    total: torch.Tensor         # [1]
+    violations: torch.Tensor    # [1]
+
+    def zero_(self) -> "AuditBuffers":
+        # fill kernels (torch's zero_), not memset nodes
+        self.token_rows.zero_()
+        self.priv_calls.zero_()
+        return self
+
+
+class PolicyMaskedMoE:
+    """One policy-masked MoE layer with weights already on the device.
+
+    Weights: wr_pub [n_pub, H] fp32, wr_priv [n_priv, H] fp32 (or None), bias [E] fp32 or
+    None, w13_* [n, 2I, H], w2_* [n, H, I] in the activation dtype, shared group
+    w13_sh [2 Is, H], w2_sh [H, Is] or None.
+    """
+
+    def __init__(self, desc: N.LayerDesc, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_priv,
+                 w2_priv, w13_sh=None, w2_sh=None, gather_in_dispatch: bool = False):
+        self.desc = desc
+        self.wr_pub, self.wr_priv, self.bias = wr_pub, wr_priv, bias
+        self.w13_pub, self.w2_pub = w13_pub, w2_pub
+        self.w13_priv, self.w2_priv = w13_priv, w2_priv
+        self.w13_sh, self.w2_sh = w13_sh, w2_sh
+        self.gather_in_dispatch = gather_in_dispatch
+        self._bufs = {}
+
+    @property
+    def device(self):
+        return self.w13_pub.device
+
+    @property
+    def act_dtype(self):
+        return torch.bfloat16 if self.desc.act_dtype == N.PMPE_BF16 else torch.float32
+
+    def buffers(self, T: int) -> LayerBuffers:
+        if T not in self._bufs:
+            d, dev, k, H = self.desc, self.device, self.desc.top_k, self.desc.hidden
+            E = d.n_pub + d.n_priv
+            i32 = dict(dtype=torch.int32, device=dev)
+            ws_bytes = max(N.pmpe_workspace_bytes(d, T), 256)
+            self._bufs[T] = LayerBuffers(
+                topk_idx=torch.empty(T * k, **i32), topk_gate=torch.empty(T * k, dtype=torch.float32, device=dev),
+                allow=torch.empty(T, dtype=torch.uint8, device=dev),
+                kgap=torch.empty(T, dtype=torch.float32, device=dev),
+                expert_count=torch.empty(E, **i32), expert_offset=torch.empty(E + 1, **i32),
+                row_token=torch.empty(T * k, **i32), token_row=torch.empty(T * k, **i32),
+                x_perm=(torch.empty(T * k, H, dtype=self.act_dtype, device=dev)
+                        if self.gather_in_dispatch else None),
+                y_perm=torch.empty(T * k, H, dtype=self.act_dtype, device=dev),
+                y_shared=(torch.empty(T, H, dtype=self.act_dtype, device=dev) if d.n_shared else None),
+                out=torch.empty(T, H, dtype=self.act_dtype, device=dev),
+                ws=torch.empty(ws_bytes, dtype=torch.uint8, device=dev),
+                dev_status=torch.zeros(1, **i32))
+        return self._bufs[T]
+
+    def audit_buffers(self, T: int, R: int) -> AuditBuffers:
+        dev = self.device
+        return AuditBuffers(torch.zeros(T, dtype=torch.int32, device=dev),
+                            torch.zeros(self.desc.n_priv, dtype=torch.int32, device=dev),
+                            torch.zeros(R, dtype=torch.int64, device=dev),
+                            torch.zeros(1, dtype=torch.int64, device=dev),
+                            torch.zeros(1, dtype=torch.int32, device=dev))
+
+    def route(self, x, words, b: LayerBuffers, stream=None):
+        T = x.shape[0]
+        N.pmpe_route(self.desc, T, x, self.wr_pub, self.wr_priv, self.bias, words, b.topk_idx,
+                     b.topk_gate, b.allow, b.kgap, b.dev_status, stream)
+
+    def dispatch(self, x, b: LayerBuffers, stream=None):
+        T = x.shape[0]
+        N.pmpe_dispatch(self.desc, T, b.topk_idx, x, b.expert_count, b.expert_offset, b.row_token,
+                        b.token_row, b.x_perm, b.ws, stream)
+
+    def expert_ffn(self, x, b: LayerBuffers, audit: AuditBuffers, stream=None):
+        T = x.shape[0]
+        N.pmpe_expert_ffn(self.desc, T, b.x_perm, x, b.expert_count, b.expert_offset, b.row_token,
+                          self.w13_pub, self.w2_pub, self.w13_priv, self.w2_priv, self.w13_sh,
+                          self.w2_sh, b.y_shared, b.y_perm, audit.token_rows, audit.priv_calls,
+                          b.dev_status, b.ws, stream)
+
+    def combine(self, x, b: LayerBuffers, stream=None):
+        T = x.shape[0]
+        N.pmpe_combine(self.desc, T, b.y_perm, b.token_row, b.topk_gate, b.y_shared, b.out, stream)
+
+    def audit(self, T: int, b: LayerBuffers, audit: AuditBuffers, req_offset, stream=None):
+        R = req_offset.numel() - 1
+        N.pmpe_audit(self.desc, T, audit.token_rows, b.allow, req_offset, R, audit.req_rows,
+                     audit.total, audit.violations, stream)
+
+    def forward(self, x, words, audit: AuditBuffers, req_offset=None, stream=None) -> LayerBuffers:
+        """Runs the layer; returns the buffers (out, route log, dispatch) of this T."""
+        b = self.buffers(x.shape[0])
+        self.route(x, words, b, stream)
+        self.dispatch(x, b, stream)
+        self.expert_ffn(x, b, audit, stream)
+        self.combine(x, b, stream)
+        if req_offset is not None:
+            self.audit(x.shape[0], b, audit, req_offset, stream)
+        return b

@@ -1,0 +1,161 @@
+"""Helpers for GPU parity tests: build a layer case from the seeded workloads, run it
+through the C ABI on the device, and run the CPU oracle on the same inputs.
+
+The oracle always receives inputs generated on the host; the device receives the
+same tensors generated on the device (the generator is bit-identical on both)."""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+import workloads as W
+from oracle import pmpe_oracle as O
+
+RTOL_BF16 = 1e-2
+RTOL_F32 = 1e-5
+RTOL_GATE = 1e-5
+
+
+def np64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to(torch.float64).cpu().numpy()
+
+
+class ExpertBank:
+    """Lazily generated host copies of one layer's expert weights, indexed by the
+    expert's index within its pool (what the oracle's containers expect)."""
+
+    def __init__(self, cfg: W.LayerConfig, layer: int, private: bool, which: str):
+        self.cfg, self.layer, self.private, self.which = cfg, layer, private, which
+        self.cache: Dict[int, np.ndarray] = {}
+
+    def __getitem__(self, i: int) -> np.ndarray:
+        if i not in self.cache:
+            e = i + (self.cfg.n_pub if self.private else 0)
+            w13, w2 = W.make_expert(self.cfg, self.layer, e, "cpu")
+            self.cache[i] = np64(w13 if self.which == "w13" else w2)
+        return self.cache[i]
+
+
+@dataclasses.dataclass
+class OracleInputs:
+    x: np.ndarray
+    wr_pub: np.ndarray
+    wr_priv: np.ndarray
+    bias: Optional[np.ndarray]
+    w13_pub: ExpertBank
+    w2_pub: ExpertBank
+    w13_priv: ExpertBank
+    w2_priv: ExpertBank
+    w13_sh: Optional[np.ndarray]
+    w2_sh: Optional[np.ndarray]
+
+
+def oracle_inputs(cfg: W.LayerConfig, layer: int = 0, x: Optional[torch.Tensor] = None) -> OracleInputs:
+    wr_pub, wr_priv, bias = W.make_router(cfg, layer, "cpu")
+    w13_sh, w2_sh = W.make_shared(cfg, layer, "cpu")
+    xx = W.make_x(cfg, "cpu") if x is None else x.cpu()
+    return OracleInputs(np64(xx), np64(wr_pub), np64(wr_priv), None if bias is None else np64(bias),
+                        ExpertBank(cfg, layer, False, "w13"), ExpertBank(cfg, layer, False, "w2"),
+                        ExpertBank(cfg, layer, True, "w13"), ExpertBank(cfg, layer, True, "w2"),
+                        None if w13_sh is None else np64(w13_sh), None if w2_sh is None else np64(w2_sh))
+
+
+def oracle_layer(cfg: W.LayerConfig, oi: OracleInputs, words: Sequence[int],
+                 tokens: Optional[Sequence[int]] = None) -> O.LayerResult:
+    return O.layer_forward(oi.x, oi.wr_pub, oi.wr_priv, oi.bias, oi.w13_pub, oi.w2_pub,
+                           oi.w13_priv, oi.w2_priv, words, cfg.top_k, cfg.gate_mode,
+                           oi.w13_sh, oi.w2_sh, tokens)
+
+
+def make_desc(cfg: W.LayerConfig):
+    import paper_2608_06690_amd as P
+    gm = P.PMPE_GATE_POOL_SOFTMAX if cfg.gate_mode == "pool_softmax" else P.PMPE_GATE_RENORM_TOPK
+    return P.make_desc(cfg.hidden, cfg.inter, cfg.n_pub, cfg.n_priv, cfg.top_k, cfg.n_shared,
+                       cfg.shared_inter, cfg.dtype == "bf16", gm)
+
+
+def device_layer(cfg: W.LayerConfig, layer: int = 0, device="cuda", gather_in_dispatch=False,
+                 drop_private: bool = False):
+    import paper_2608_06690_amd as P
+    Lw = W.make_layer(cfg, layer, device)
+    priv = (lambda t: None) if drop_private else (lambda t: t)
+    return P.PolicyMaskedMoE(make_desc(cfg), Lw.wr_pub, priv(Lw.wr_priv), Lw.bias, Lw.w13_pub,
+                             Lw.w2_pub, priv(Lw.w13_priv), priv(Lw.w2_priv), Lw.w13_sh, Lw.w2_sh,
+                             gather_in_dispatch=gather_in_dispatch), Lw
+
+
+def words_tensor(words: Sequence[int], device="cuda") -> torch.Tensor:
+    return torch.from_numpy(np.asarray(words, np.uint32).view(np.int32).copy()).to(device)
+
+
+@dataclasses.dataclass
+class DeviceResult:
+    idx: np.ndarray
+    gate: np.ndarray
+    allow: np.ndarray
+    kgap: np.ndarray
+    count: np.ndarray
+    offset: np.ndarray
+    row_token: np.ndarray
+    token_row: np.ndarray
+    out: torch.Tensor          # on host, act dtype
+    audit_rows: np.ndarray
+    audit_calls: np.ndarray
+    req_rows: np.ndarray
+    total: int
+    violations: int
+    dev_status: int
+
+
+def run_device(layer, x: torch.Tensor, words: Optional[torch.Tensor], req_offset: torch.Tensor,
+               audit=None) -> DeviceResult:
+    T = x.shape[0]
+    R = req_offset.numel() - 1
+    k = layer.desc.top_k
+    audit = audit or layer.audit_buffers(T, R)
+    b = layer.forward(x, words, audit, req_offset)
+    torch.cuda.synchronize()
+    u32 = lambda t: t.cpu().numpy().view(np.uint32).astype(np.int64)  # noqa: E731
+    return DeviceResult(
+        idx=b.topk_idx.view(T, k).cpu().numpy().astype(np.int64),
+        gate=b.topk_gate.view(T, k).cpu().numpy(), allow=b.allow.cpu().numpy(),
+        kgap=b.kgap.cpu().numpy(), count=b.expert_count.cpu().numpy().astype(np.int64),
+        offset=b.expert_offset.cpu().numpy().astype(np.int64),
+        row_token=b.row_token.cpu().numpy().astype(np.int64),
+        token_row=b.token_row.view(T, k).cpu().numpy().astype(np.int64),
+        out=b.out.cpu().clone(), audit_rows=u32(audit.token_rows), audit_calls=u32(audit.priv_calls),
+        req_rows=audit.req_rows.cpu().numpy(), total=int(audit.total.item()),
+        violations=int(audit.violations.item()), dev_status=int(b.dev_status.item()))
+
+
+def rel_l2(a: np.ndarray, b: np.ndarray) -> float:
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a - b))
+
+
+def check_dispatch_consistent(d: DeviceResult, E: int) -> None:
+    """Dispatch outputs are pure functions of the device's own topk_idx."""
+    ref = O.dispatch(d.idx, E)
+    assert np.array_equal(d.count, ref.count)
+    assert np.array_equal(d.offset, ref.offset)
+    assert np.array_equal(d.row_token, ref.row_token)
+    assert np.array_equal(d.token_row, ref.token_row)
+
+
+def compare_routes(cfg, d: DeviceResult, rt: O.Route, tokens=None) -> Dict[str, int]:
+    """Routing parity: allow bit-exact everywhere; idx bit-exact off near-ties; gates
+    within RTOL_GATE on tokens whose idx agree. Returns near-tie statistics."""
+    toks = np.arange(d.idx.shape[0]) if tokens is None else np.asarray(tokens)
+    assert np.array_equal(d.allow[toks], rt.allow[toks])
+    nt = rt.near_tie[toks]
+    same = np.all(d.idx[toks] == rt.idx[toks], axis=1)
+    bad = toks[~same & ~nt]
+    assert bad.size == 0, f"routing differs on non-near-tie tokens {bad[:10]}"
+    ok = toks[same]
+    assert rel_l2(d.gate[ok], rt.gate[ok]) <= RTOL_GATE
+    return {"near_tie": int(nt.sum()), "near_tie_differ": int((~same & nt).sum()), "agree": int(same.sum())}

@@ -1,0 +1,145 @@
+"""C ABI checks that need no GPU: every symbol declared in include/pmpe.h is exported,
+the binding's argument lists match the declarations, and host-side validation
+returns the documented status before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_06690_amd as P
+from paper_2608_06690_amd import _native as N
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pmpe.h")
+
+
+def declarations():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    decls = {}
+    for m in re.finditer(r"\b(?:pmpe_status|size_t|const char\*|int32_t)\s+(pmpe_\w+)\s*\(([^)]*)\)\s*;", src):
+        params = [p.strip() for p in m.group(2).split(",") if p.strip() and p.strip() != "void"]
+        decls[m.group(1)] = params
+    return decls
+
+
+def test_header_declares_the_five_calls():
+    d = declarations()
+    for name in ["pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
+                 "pmpe_workspace_bytes", "pmpe_status_string", "pmpe_version", "pmpe_check_desc"]:
+        assert name in d, name
+
+
+def test_every_declared_symbol_is_exported():
+    lib = N.lib()
+    for name in declarations():
+        assert hasattr(lib, name), name
+        assert isinstance(getattr(lib, name), ctypes._CFuncPtr)
+
+
+def test_binding_argument_counts_match_header():
+    lib = N.lib()
+    for name, params in declarations().items():
+        assert len(getattr(lib, name).argtypes) == len(params), name
+
+
+def desc(**kw):
+    base = dict(hidden=2048, inter=768, n_pub=128, n_priv=32, top_k=8)
+    base.update(kw)
+    return P.make_desc(**base)
+
+
+def test_valid_descriptor_and_workspace():
+    d = desc()
+    assert P.pmpe_check_desc(d, 4096) == 0
+    ws = P.pmpe_workspace_bytes(d, 4096)
+    assert ws >= 4096 * 8 * 768 * 2          # the SwiGLU intermediate of every row
+    assert P.pmpe_workspace_bytes(d, 0) >= 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(top_k=9, n_priv=8), -3), (dict(top_k=129), -2), (dict(top_k=0), -2),
+    (dict(hidden=100), -2), (dict(hidden=192), -2), (dict(inter=100), -2),
+    (dict(n_pub=0), -2), (dict(n_pub=300), -2), (dict(n_priv=300), -2),
+    (dict(n_shared=2, shared_inter=0), -2),
+])
+def test_invalid_descriptor_codes(kw, status):
+    d = desc(**kw)
+    assert P.pmpe_check_desc(d, 16) == status
+    assert P.pmpe_workspace_bytes(d, 16) == 0
+
+
+def test_dtype_and_gate_mode_codes():
+    d = desc()
+    d.w_dtype = N.PMPE_F32
+    assert P.pmpe_check_desc(d, 16) == -4
+    d = desc()
+    d.act_dtype = d.w_dtype = 7
+    assert P.pmpe_check_desc(d, 16) == -4
+    d = desc()
+    d.gate_mode = 5
+    assert P.pmpe_check_desc(d, 16) == -2
+    assert P.pmpe_check_desc(desc(), -1) == -2
+
+
+def fake(addr):
+    """A pointer-like stand-in: never dereferenced, validation fails before launch."""
+    class F:
+        def is_contiguous(self):
+            return True
+
+        def data_ptr(self):
+            return addr
+    return F()
+
+
+def test_null_and_alignment_rejected_before_launch():
+    d = desc()
+    lib = N.lib()
+    # NULL x
+    st = lib.pmpe_route(ctypes.byref(d), 16, None, 0x1000, None, None, None, 0x2000, 0x3000, 0x4000,
+                        None, None, None)
+    assert st == -1
+    # misaligned x
+    st = lib.pmpe_route(ctypes.byref(d), 16, 0x1004, 0x1000, None, None, None, 0x2000, 0x3000,
+                        0x4000, None, None, None)
+    assert st == -5
+    # dispatch without workspace
+    st = lib.pmpe_dispatch(ctypes.byref(d), 16, 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000,
+                           None, None, 0, None)
+    assert st == -6
+    # expert ffn with a too small workspace
+    st = lib.pmpe_expert_ffn(ctypes.byref(d), 16, 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000,
+                             0x7000, None, None, None, None, None, 0x8000, 0x9000, None, None,
+                             0xA000, 16, None)
+    assert st == -6
+    # shared experts requested but not given
+    d2 = desc(n_shared=2, shared_inter=1408)
+    st = lib.pmpe_combine(ctypes.byref(d2), 16, 0x1000, 0x2000, 0x3000, None, 0x4000, None)
+    assert st == -1
+    # audit: negative request count
+    st = lib.pmpe_audit(ctypes.byref(d), 16, 0x1000, 0x2000, 0x3000, -1, 0x4000, 0x5000, 0x6000, None)
+    assert st == -2
+
+
+def test_zero_tokens_launch_nothing():
+    d = desc()
+    lib = N.lib()
+    assert lib.pmpe_route(ctypes.byref(d), 0, 0x1000, 0x1000, None, None, None, 0x2000, 0x3000,
+                          0x4000, None, None, None) == 0
+    assert lib.pmpe_combine(ctypes.byref(d), 0, 0x1000, 0x2000, 0x3000, None, 0x4000, None) == 0
+
+
+def test_status_strings():
+    for s in range(-7, 1):
+        assert N.lib().pmpe_status_string(s).decode()
+    assert P.pmpe_version() >= 10000
+
+
+def test_policy_resolver_product_side():
+    import workloads as W
+    assert P.resolve_policy({"allow_private": True})
+    for m in W.MALFORMED_META:
+        assert not P.resolve_policy(m)
+    w = P.token_policy_words([{"allow_private": True}, None], [2, 1])
+    assert [int(v) & 0xFFFFFFFF for v in w] == [N.PMPE_POLICY_ALLOW] * 2 + [0]
