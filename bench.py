@@ -1,0 +1,238 @@
+"""Benchmark of the policy-masked MoE layer forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-decode]
+
+A step is one pass of the whole layer (route, dispatch, expert FFN, combine, audit)
+over the Qwen3-30B-A3B-shaped workload: 4096 tokens in 8 requests of 512 (4 allow,
+4 deny), H 2048, I 768, 128 public + 32 private experts, top-8, bf16 experts, fp32
+router; inputs synthetic and resident in HBM. Prints one JSON line.
+
+Per-call times come from HIP events recorded on the stream the library launches on.
+The roofline object describes pmpe_expert_ffn (the dominant call): its algorithmic
+flops are 2 * 3 * H * I per (token, expert) pair. The CPU baseline is the CPU oracle
+timed on a bounded sample of the same workload on this host's cores. The decode
+object is the 256-request single-token workload, whose expert FFN is bound by HBM
+reads of the touched experts' weights.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s (Qwen3-30B-A3B shape) + % MFMA peak; decode % HBM BW"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+CALLS = ["route", "dispatch", "expert_ffn", "combine", "audit"]
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode", action="store_true")
+    p.add_argument("--cpu-sample", type=int, default=4096, help="tokens in the CPU-oracle sample")
+    p.add_argument("--cpu-reps", type=int, default=3, help="timed repetitions of the CPU oracle")
+    p.add_argument("--decode-only", action="store_true",
+                   help="time only the decode workload (for a separate kernel profile)")
+    return p.parse_args()
+
+
+def setup(cfg_name, device):
+    import torch
+    import workloads as W
+    import paper_2608_06690_amd as P
+
+    cfg = W.get_config(cfg_name)
+    Lw = W.make_layer(cfg, 0, device)
+    gm = P.PMPE_GATE_POOL_SOFTMAX if cfg.gate_mode == "pool_softmax" else P.PMPE_GATE_RENORM_TOPK
+    desc = P.make_desc(cfg.hidden, cfg.inter, cfg.n_pub, cfg.n_priv, cfg.top_k, cfg.n_shared,
+                       cfg.shared_inter, cfg.dtype == "bf16", gm)
+    layer = P.PolicyMaskedMoE(desc, Lw.wr_pub, Lw.wr_priv, Lw.bias, Lw.w13_pub, Lw.w2_pub,
+                              Lw.w13_priv, Lw.w2_priv, Lw.w13_sh, Lw.w2_sh)
+    x = W.make_x(cfg, device)
+    req = W.make_requests(cfg, 0)
+    words = P.token_policy_words(req.metas, req.lengths, device)
+    req_off = P.request_offsets(req.lengths, device)
+    audit = layer.audit_buffers(cfg.tokens, len(req.lengths))
+    bufs = layer.buffers(cfg.tokens)
+    torch.cuda.synchronize()
+    return cfg, layer, x, words, req_off, audit, bufs, req
+
+
+def run_step(layer, x, words, req_off, audit, bufs, stream, events=None):
+    """One layer pass; with `events` (6 events) records a boundary around every call."""
+    T = x.shape[0]
+    if events:
+        events[0].record(stream)
+    layer.route(x, words, bufs, stream)
+    if events:
+        events[1].record(stream)
+    layer.dispatch(x, bufs, stream)
+    if events:
+        events[2].record(stream)
+    layer.expert_ffn(x, bufs, audit, stream)
+    if events:
+        events[3].record(stream)
+    layer.combine(x, bufs, stream)
+    if events:
+        events[4].record(stream)
+    layer.audit(T, bufs, audit, req_off, stream)
+    if events:
+        events[5].record(stream)
+
+
+def time_layer(layer, x, words, req_off, audit, bufs, steps, warmup, flush=None):
+    import torch
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        audit.zero_()
+        run_step(layer, x, words, req_off, audit, bufs, stream)
+    torch.cuda.synchronize()
+    # whole-step throughput: K back-to-back steps
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run_step(layer, x, words, req_off, audit, bufs, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    # per-call durations from events on the launch stream
+    per = {c: [] for c in CALLS}
+    for _ in range(steps):
+        if flush is not None:
+            flush.fill_(1)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        run_step(layer, x, words, req_off, audit, bufs, stream, ev)
+        torch.cuda.synchronize()
+        for i, c in enumerate(CALLS):
+            per[c].append(ev[i].elapsed_time(ev[i + 1]) * 1e3)  # us
+    med = {c: sorted(v)[len(v) // 2] for c, v in per.items()}
+    mean = {c: sum(v) / len(v) for c, v in per.items()}
+    return wall / steps * 1e3, med, mean
+
+
+def cpu_baseline(cfg, req, n_sample, reps):
+    """The CPU oracle on a bounded sample: n_sample tokens (half from allow requests,
+    half from deny requests), routed and run through their experts; the median of
+    `reps` timed repetitions."""
+    import numpy as np
+    import torch
+    from oracle import pmpe_oracle as O
+    import workloads as W
+
+    torch.set_num_threads(len(os.sched_getaffinity(0)))
+    words_all = O.compile_words(req.metas, req.lengths)
+    rng = np.random.default_rng(0)
+    allow_t = np.nonzero(words_all == O.ALLOW_WORD)[0]
+    deny_t = np.nonzero(words_all != O.ALLOW_WORD)[0]
+    toks = np.sort(np.concatenate([rng.choice(allow_t, n_sample // 2, replace=False),
+                                   rng.choice(deny_t, n_sample - n_sample // 2, replace=False)]))
+    x = W.make_x(cfg, "cpu")[torch.as_tensor(toks)].double().numpy()
+    wr_pub, wr_priv, bias = (t.double().numpy() if t is not None else None for t in W.make_router(cfg))
+    w13 = np.empty((cfg.n_experts, 2 * cfg.inter, cfg.hidden))
+    w2 = np.empty((cfg.n_experts, cfg.hidden, cfg.inter))
+    for e in range(cfg.n_experts):  # inputs resident before timing
+        a, b = W.make_expert(cfg, 0, e, "cpu")
+        w13[e] = a.double().numpy()
+        w2[e] = b.double().numpy()
+    words = words_all[toks]
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        res = O.layer_forward(x, wr_pub, wr_priv, bias, w13[:cfg.n_pub], w2[:cfg.n_pub],
+                              w13[cfg.n_pub:], w2[cfg.n_pub:], words, cfg.top_k, cfg.gate_mode)
+        O.audit(res.hook.rows, res.route.allow, [0, len(toks)])
+        times.append(time.perf_counter() - t0)
+    dt = sorted(times)[len(times) // 2]
+    return {"value": len(toks) / dt, "unit": "tokens/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"{len(toks)} of the {cfg.tokens} tokens ({n_sample // 2} allow, "
+                      f"{n_sample - n_sample // 2} deny), whole layer in fp64 numpy; median of "
+                      f"{reps} runs, {dt:.1f} s each"}
+
+
+def decode_bench(args, dev):
+    """The decode workload: tokens/s and the expert FFN's HBM rate on the touched
+    experts' weights (each read once per call), with L2/MALL flushed before each
+    event-timed step."""
+    import torch
+    cfgd, layerd, xd, wd, rod, ad, bd, _ = setup("decode", dev)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    msd, medd, meand = time_layer(layerd, xd, wd, rod, ad, bd, args.steps, args.warmup, flush)
+    counts = bd.expert_count.cpu()
+    touched = int((counts > 0).sum())
+    wb = touched * 3 * cfgd.hidden * cfgd.inter * 2
+    gbs = wb / (meand["expert_ffn"] * 1e-6) / 1e9
+    res = {"workload": "qwen3-30b-a3b-shaped decode layer, 256 requests x 1 token",
+           "tokens_per_s": cfgd.tokens / (msd * 1e-3), "ms_per_step": msd,
+           "experts_touched": touched, "weight_bytes": wb,
+           "ffn_us_mean": meand["expert_ffn"], "ffn_hbm_gbs": gbs,
+           "ffn_hbm_frac": gbs / PEAK_HBM_GBS, "calls_us_mean": meand,
+           "note": "L2/MALL flushed by a 512 MiB write before each event-timed step"}
+    del layerd, xd, bd, flush
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the layer is single-GPU and no multi-GPU path is "
+              f"built (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads as W
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    if args.decode_only:
+        print(json.dumps(decode_bench(args, dev)), flush=True)
+        return
+    cfg, layer, x, words, req_off, audit, bufs, req = setup("qwen", dev)
+    ms, med, mean = time_layer(layer, x, words, req_off, audit, bufs, args.steps, args.warmup)
+    T = cfg.tokens
+    pairs = T * cfg.top_k
+    ffn_flop = pairs * 2 * 3 * cfg.hidden * cfg.inter
+    w_bytes = cfg.n_experts * 3 * cfg.hidden * cfg.inter * 2
+    ffn_us = mean["expert_ffn"]
+    achieved = ffn_flop / (ffn_us * 1e-6) / 1e12
+    ai = ffn_flop / w_bytes
+    attainable = min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3)
+    out = {
+        "metric": METRIC, "value": T / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "qwen3-30b-a3b-shaped policy-masked moe layer", "tokens": T,
+                   "requests": cfg.requests, "hidden": cfg.hidden, "inter": cfg.inter,
+                   "n_pub": cfg.n_pub, "n_priv": cfg.n_priv, "top_k": cfg.top_k,
+                   "policy": "4 allow + 4 deny requests", "router": "fp32", "experts": "bf16"},
+        "roofline": {"kernel": "pmpe_expert_ffn (gemm1_bf16_kernel + gemm2_bf16_kernel)",
+                     "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flop_per_launch": ffn_flop, "avg_us": ffn_us,
+                     "weight_bytes": w_bytes, "ai_flop_per_weight_byte": ai,
+                     "attainable_tflops_at_hbm_peak": attainable,
+                     "attainable_frac": achieved / attainable},
+        "calls_us_mean": mean, "calls_us_median": med,
+    }
+    del layer, x, bufs
+    torch.cuda.empty_cache()
+
+    if not args.no_decode:
+        out["decode"] = decode_bench(args, dev)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, req, args.cpu_sample, args.cpu_reps)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -30,7 +30,8 @@
  *   see (e.g. private rows reaching a NULL private weight pointer) set bits in the
  *   optional `dev_status` word.
  * - Calls are stream-ordered; a workspace may be shared by calls on one stream.
- * - T = 0 is valid: nothing is launched and PMPE_OK is returned.
+ * - T = 0 is valid: nothing is launched and PMPE_OK is returned (pmpe_audit still
+ *   writes its outputs).
  * - Row-major layouts throughout. Expert ids: public [0, n_pub), private
  *   [n_pub, n_pub + n_priv).
  * - No C++ exception crosses this ABI.
@@ -83,7 +84,7 @@ typedef enum { PMPE_GATE_RENORM_TOPK = 0, PMPE_GATE_POOL_SOFTMAX = 1 } pmpe_gate
 #define PMPE_MAX_TOKENS (1 << 24)
 
 typedef struct {
-  int32_t hidden;       /* H, multiple of 64, <= 16384 */
+  int32_t hidden;       /* H, multiple of 128, 128..16384 */
   int32_t inter;        /* I of one routed expert, multiple of 64 */
   int32_t n_pub;        /* public (original, frozen) experts */
   int32_t n_priv;       /* private (added) experts */
@@ -105,8 +106,8 @@ const char* pmpe_status_string(int32_t status);
 /* Library version, major * 10000 + minor * 100 + patch. */
 int32_t pmpe_version(void);
 
-/* Validation only: returns what pmpe_route would return for these arguments, without
- * launching. Lets a host without a GPU check arguments. */
+/* Validation only: PMPE_OK if the descriptor and T are supported, else the status every
+ * call would return for them. Launches nothing, so it also runs on a host without a GPU. */
 pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T);
 
 /*
@@ -134,11 +135,13 @@ pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T);
  *   kgap         [T] fp32 out or NULL: k-th minus (k+1)-th largest masked logit,
  *                +inf when the pool has exactly k experts
  *   dev_status   [1] uint32 in/out or NULL: status bits are OR-ed in
+ *   ws, ws_bytes workspace (holds the fp32 pool logits), at least
+ *                pmpe_workspace_bytes(d, T)
  */
 pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const float* wr_pub,
                        const float* wr_priv, const float* logit_bias, const uint32_t* policy_word,
                        int32_t* topk_idx, float* topk_gate, uint8_t* allow, float* kgap,
-                       uint32_t* dev_status, pmpe_stream_t stream);
+                       uint32_t* dev_status, void* ws, size_t ws_bytes, pmpe_stream_t stream);
 
 /*
  * pmpe_dispatch - group the T*k (token, expert) pairs by expert.
@@ -230,7 +233,8 @@ pmpe_status pmpe_combine(const pmpe_layer_desc* d, int32_t T, const void* y_perm
  *                      req_offset[R] = T (a device array)
  *   req_private_rows   [R] uint64 out
  *   total_private_rows [1] uint64 out
- *   deny_violations    [1] uint32 out: tokens with allow == 0 and a nonzero count
+ *   deny_violations    [1] uint32 out: tokens inside the requests with allow == 0 and
+ *                      a nonzero count
  */
 pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audit_token_rows,
                        const uint8_t* allow, const int32_t* req_offset, int32_t R,

@@ -14,7 +14,8 @@ from typing import Optional
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libpmpe.so")
+# PMPE_LIB_PATH selects another build of the same library (e.g. a tuning variant).
+LIB_PATH = os.environ.get("PMPE_LIB_PATH") or os.path.join(_PKG, "libpmpe.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(
@@ -66,7 +67,7 @@ _lib.pmpe_workspace_bytes.argtypes = [_DESC, _I32]
 _lib.pmpe_check_desc.restype = _I32
 _lib.pmpe_check_desc.argtypes = [_DESC, _I32]
 _lib.pmpe_route.restype = _I32
-_lib.pmpe_route.argtypes = [_DESC, _I32] + [_P] * 10 + [_P]
+_lib.pmpe_route.argtypes = [_DESC, _I32] + [_P] * 10 + [_P, _SZ, _P]
 _lib.pmpe_dispatch.restype = _I32
 _lib.pmpe_dispatch.argtypes = [_DESC, _I32] + [_P] * 7 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn.restype = _I32
@@ -123,10 +124,12 @@ def pmpe_check_desc(desc: LayerDesc, T: int) -> int:
 
 
 def pmpe_route(desc, T, x, wr_pub, wr_priv, logit_bias, policy_word, topk_idx, topk_gate, allow,
-               kgap=None, dev_status=None, stream=None) -> None:
+               kgap, dev_status, ws, stream=None) -> None:
     _check(_lib.pmpe_route(ctypes.byref(desc), T, _ptr(x), _ptr(wr_pub), _ptr(wr_priv),
                            _ptr(logit_bias), _ptr(policy_word), _ptr(topk_idx), _ptr(topk_gate),
-                           _ptr(allow), _ptr(kgap), _ptr(dev_status), _stream(stream)), "pmpe_route")
+                           _ptr(allow), _ptr(kgap), _ptr(dev_status), _ptr(ws),
+                           0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
+           "pmpe_route")
 
 
 def pmpe_dispatch(desc, T, topk_idx, x, expert_count, expert_offset, row_token, token_row, x_perm,

@@ -1,17 +1,20 @@
 // K2 - dispatch: group the T*k (token, expert) pairs by expert, stably.
 //
-// Pairs are numbered token-major, p = t*k + j. A stable counting sort by expert id
-// gives each expert's rows in ascending token order:
-//  rank     one workgroup per chunk of 64 tokens: each pair's rank among the earlier
-//           pairs of the chunk with the same expert (an in-order count, so the order is
-//           deterministic) and the chunk's per-expert histogram (LDS atomics; integer
-//           counts do not depend on the atomics' order).
-//  scan     one workgroup: per expert, the running sum over chunks gives each chunk's
-//           base; expert_count; exclusive scan over experts gives expert_offset.
-//  scatter  row = offset[e] + chunk base + rank; token_row[p] = row; row_token[row] = t.
-//  gather   (optional) one wave per permuted row copies x[row_token[row]] to x_perm[row]:
-//           whole 16-byte-vector rows, so reads and writes are coalesced.
-// Expert ids outside [0, E) are not counted and get token_row = -1.
+// Tokens are cut into chunks of 64. A stable counting sort by expert id gives every
+// expert its rows in ascending token order:
+//  hist     one workgroup per chunk builds, for every expert, the 64-bit mask of the
+//           chunk's tokens that selected it (LDS 64-bit atomic OR: the result does not
+//           depend on the order of the atomics). popcount(mask) is the chunk's
+//           histogram, and the rank of token t among the chunk's rows of expert e is
+//           popcount(mask_e & ((1 << t) - 1)).
+//  scan     one workgroup per expert: the expert's offset is the number of pairs of
+//           all lower experts; a scan over the chunks' counts gives each chunk's first
+//           row; expert_count and expert_offset are written.
+//  scatter  row = chunk base + rank; token_row[t*k+j] = row; row_token[row] = t.
+//  gather   (optional) one wave per permuted row copies x[row_token[row]] to
+//           x_perm[row] in 16-byte vectors, so reads and writes are coalesced.
+// No order-dependent atomics: the permutation is deterministic. Expert ids outside
+// [0, E) are not counted and get token_row = -1.
 #include "pmpe_internal.h"
 
 namespace pmpe {
@@ -21,67 +24,63 @@ constexpr int DP_TOK = 64;
 constexpr int DP_THREADS = 256;
 constexpr int DP_MAX_E = 2 * PMPE_MAX_POOL;
 
-__global__ __launch_bounds__(DP_THREADS) void dispatch_rank_kernel(DispatchArgs a) {
-  __shared__ int s_key[DP_TOK * PMPE_MAX_TOPK];
-  __shared__ int s_hist[DP_MAX_E];
+__device__ __forceinline__ int popc64(uint64_t v) { return __popcll(v); }
+
+__global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(DispatchArgs a) {
+  __shared__ unsigned long long s_mask[DP_MAX_E];
   const int tid = threadIdx.x;
   const int c = blockIdx.x;
   const int t0 = c * DP_TOK;
-  const int ntok = min(DP_TOK, a.T - t0);
-  const int np = ntok * a.k;
+  const int np = min(DP_TOK, a.T - t0) * a.k;
   const size_t p0 = (size_t)t0 * a.k;
-  for (int e = tid; e < a.E; e += DP_THREADS) s_hist[e] = 0;
+  for (int e = tid; e < a.E; e += DP_THREADS) s_mask[e] = 0ull;
+  __syncthreads();
   for (int i = tid; i < np; i += DP_THREADS) {
     const int e = a.topk_idx[p0 + i];
-    s_key[i] = (e >= 0 && e < a.E) ? e : -1;
+    if (e >= 0 && e < a.E) atomicOr(&s_mask[e], 1ull << (i / a.k));
   }
   __syncthreads();
-  for (int i = tid; i < np; i += DP_THREADS) {
-    const int key = s_key[i];
-    int r = -1;
-    if (key >= 0) {
-      r = 0;
-      for (int q = 0; q < i; ++q) r += (s_key[q] == key) ? 1 : 0;
-      atomicAdd(&s_hist[key], 1);
-    }
-    a.rank[p0 + i] = r;
-  }
-  __syncthreads();
-  for (int e = tid; e < a.E; e += DP_THREADS) a.chunk_base[(size_t)c * a.E + e] = s_hist[e];
+  for (int e = tid; e < a.E; e += DP_THREADS) a.mask[(size_t)c * a.E + e] = s_mask[e];
 }
 
-constexpr int SC_THREADS = 1024;
-
-__global__ __launch_bounds__(SC_THREADS) void dispatch_scan_kernel(DispatchArgs a, int nchunks) {
-  __shared__ int s_tot[SC_THREADS];
-  const int tid = threadIdx.x;
+__global__ __launch_bounds__(DP_THREADS) void dispatch_scan_kernel(DispatchArgs a, int nchunks) {
+  __shared__ int s_red[DP_THREADS / 64];
+  __shared__ int s_wsum[DP_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int e = blockIdx.x;
   const int E = a.E;
-  // per expert: running sum over chunks (chunk counts -> chunk bases, in place)
-  int tot = 0;
-  if (tid < E) {
-    for (int c = 0; c < nchunks; ++c) {
-      const size_t i = (size_t)c * E + tid;
-      const int v = a.chunk_base[i];
-      a.chunk_base[i] = tot;
-      tot += v;
-    }
-    a.count[tid] = tot;
+  // offset[e]: all pairs of experts below e
+  int below = 0;
+  for (int i = tid; i < nchunks * e; i += DP_THREADS) {
+    const int c = i / e, ee = i - c * e;
+    below += popc64(a.mask[(size_t)c * E + ee]);
   }
-  s_tot[tid] = (tid < E) ? tot : 0;
+  for (int off = 32; off > 0; off >>= 1) below += __shfl_xor(below, off, 64);
+  if (lane == 0) s_red[wave] = below;
   __syncthreads();
-  // inclusive Hillis-Steele scan over experts
-  for (int off = 1; off < SC_THREADS; off <<= 1) {
-    const int v = (tid >= off) ? s_tot[tid - off] : 0;
+  int offset = 0;
+  for (int w = 0; w < DP_THREADS / 64; ++w) offset += s_red[w];
+  // this expert's column: exclusive scan of the chunk counts, DP_THREADS chunks at a time
+  int running = offset;
+  for (int c0 = 0; c0 < nchunks; c0 += DP_THREADS) {
+    const int c = c0 + tid;
+    const int v = (c < nchunks) ? popc64(a.mask[(size_t)c * E + e]) : 0;
+    const int incl = wave_incl_scan(v);
+    if (lane == 63) s_wsum[wave] = incl;
     __syncthreads();
-    s_tot[tid] += v;
+    int before = running;
+    for (int w = 0; w < wave; ++w) before += s_wsum[w];
+    if (c < nchunks) a.chunk_base[(size_t)c * E + e] = before + incl - v;
+    int tot = 0;
+    for (int w = 0; w < DP_THREADS / 64; ++w) tot += s_wsum[w];
+    running += tot;
     __syncthreads();
   }
-  if (tid < E) {
-    const int excl = s_tot[tid] - tot;
-    a.offset[tid] = excl;
-    for (int c = 0; c < nchunks; ++c) a.chunk_base[(size_t)c * E + tid] += excl;
+  if (tid == 0) {
+    a.count[e] = running - offset;
+    a.offset[e] = offset;
+    if (e == E - 1) a.offset[E] = running;
   }
-  if (tid == E - 1) a.offset[E] = s_tot[tid];
 }
 
 __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchArgs a) {
@@ -92,12 +91,13 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchAr
   const size_t p0 = (size_t)t0 * a.k;
   for (int i = tid; i < np; i += DP_THREADS) {
     const size_t p = p0 + i;
-    const int r = a.rank[p];
+    const int e = a.topk_idx[p];
     int row = -1;
-    if (r >= 0) {
-      const int e = a.topk_idx[p];
-      row = a.chunk_base[(size_t)c * a.E + e] + r;
-      a.row_token[row] = (int32_t)(p / a.k);
+    if (e >= 0 && e < a.E) {
+      const int tl = i / a.k;
+      const uint64_t below = (tl == 0) ? 0ull : (a.mask[(size_t)c * a.E + e] & ((1ull << tl) - 1ull));
+      row = a.chunk_base[(size_t)c * a.E + e] + popc64(below);
+      a.row_token[row] = t0 + tl;
     }
     a.token_row[p] = row;
   }
@@ -124,8 +124,8 @@ int dispatch_chunks(int T) { return (T + DP_TOK - 1) / DP_TOK; }
 
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
   const int nchunks = dispatch_chunks(a.T);
-  hipLaunchKernelGGL(dispatch_rank_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
-  hipLaunchKernelGGL(dispatch_scan_kernel, dim3(1), dim3(SC_THREADS), 0, s, a, nchunks);
+  hipLaunchKernelGGL(dispatch_hist_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
+  hipLaunchKernelGGL(dispatch_scan_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
   hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
   if (a.x_perm) {
     const int nrows = a.T * a.k;

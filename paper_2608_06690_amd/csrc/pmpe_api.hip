@@ -38,9 +38,15 @@ pmpe_status check_desc(const pmpe_layer_desc* d, int32_t T) {
   return PMPE_OK;
 }
 
+int route_zstride(const pmpe_layer_desc* d) { return d->n_pub > d->n_priv ? d->n_pub : d->n_priv; }
+
+size_t route_ws(const pmpe_layer_desc* d, int32_t T) {
+  return round_up((size_t)T * route_zstride(d) * 4);
+}
+
 size_t dispatch_ws(const pmpe_layer_desc* d, int32_t T) {
   const size_t E = (size_t)d->n_pub + d->n_priv;
-  return round_up((size_t)dispatch_chunks(T) * E * 4) + round_up((size_t)T * d->top_k * 4);
+  return round_up((size_t)dispatch_chunks(T) * E * 8) + round_up((size_t)dispatch_chunks(T) * E * 4);
 }
 
 size_t ffn_ws(const pmpe_layer_desc* d, int32_t T) {
@@ -75,22 +81,26 @@ pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T) { return check_
 
 size_t pmpe_workspace_bytes(const pmpe_layer_desc* d, int32_t T) {
   if (check_desc(d, T) != PMPE_OK) return 0;
-  const size_t a = dispatch_ws(d, T), b = ffn_ws(d, T);
-  return a > b ? a : b;
+  size_t m = route_ws(d, T);
+  if (dispatch_ws(d, T) > m) m = dispatch_ws(d, T);
+  if (ffn_ws(d, T) > m) m = ffn_ws(d, T);
+  return m;
 }
 
 pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const float* wr_pub,
                        const float* wr_priv, const float* logit_bias, const uint32_t* policy_word,
                        int32_t* topk_idx, float* topk_gate, uint8_t* allow, float* kgap,
-                       uint32_t* dev_status, pmpe_stream_t stream) {
+                       uint32_t* dev_status, void* ws, size_t ws_bytes, pmpe_stream_t stream) {
   pmpe_status st = check_desc(d, T);
   if (st != PMPE_OK) return st;
   if (!x || !wr_pub || !topk_idx || !topk_gate || !allow) return PMPE_ERR_NULL;
   if (!aligned16(x) || !aligned16(wr_pub) || (wr_priv && !aligned16(wr_priv))) return PMPE_ERR_ALIGN;
   if (T == 0) return PMPE_OK;
+  if (!ws || ws_bytes < route_ws(d, T)) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
   RouteArgs a{T, d->hidden, d->n_pub, d->n_priv, d->top_k, d->gate_mode,
               d->act_dtype == PMPE_BF16, x, wr_pub, wr_priv, logit_bias, policy_word,
-              topk_idx, topk_gate, allow, kgap, dev_status};
+              topk_idx, topk_gate, allow, kgap, dev_status, (float*)ws, route_zstride(d)};
   return launched(launch_route(a, (hipStream_t)stream));
 }
 
@@ -107,10 +117,10 @@ pmpe_status pmpe_dispatch(const pmpe_layer_desc* d, int32_t T, const int32_t* to
   if (!ws || ws_bytes < dispatch_ws(d, T)) return PMPE_ERR_WORKSPACE;
   if (!aligned16(ws)) return PMPE_ERR_ALIGN;
   const int E = d->n_pub + d->n_priv;
-  int32_t* chunk_base = (int32_t*)ws;
-  int32_t* rank = (int32_t*)((char*)ws + round_up((size_t)dispatch_chunks(T) * E * 4));
+  uint64_t* mask = (uint64_t*)ws;
+  int32_t* chunk_base = (int32_t*)((char*)ws + round_up((size_t)dispatch_chunks(T) * E * 8));
   DispatchArgs a{T, d->top_k, E, d->hidden, d->act_dtype == PMPE_BF16, topk_idx, x,
-                 expert_count, expert_offset, row_token, token_row, x_perm, chunk_base, rank};
+                 expert_count, expert_offset, row_token, token_row, x_perm, mask, chunk_base};
   return launched(launch_dispatch(a, (hipStream_t)stream));
 }
 

@@ -86,6 +86,8 @@ struct RouteArgs {
   uint8_t* allow;
   float* kgap;
   uint32_t* dev_status;
+  float* z;     // workspace [T, zstride]: fp32 logits of each token's permitted pool
+  int zstride;
 };
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 
@@ -98,8 +100,8 @@ struct DispatchArgs {
   int32_t* row_token;
   int32_t* token_row;
   void* x_perm;
-  int32_t* chunk_base;  // workspace [nchunks, E]
-  int32_t* rank;        // workspace [T*k]
+  uint64_t* mask;       // workspace [nchunks, E]: tokens of a chunk that selected an expert
+  int32_t* chunk_base;  // workspace [nchunks, E]: first row of a chunk's tokens per expert
 };
 int dispatch_chunks(int T);
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s);

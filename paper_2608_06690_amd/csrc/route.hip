@@ -22,8 +22,7 @@
 namespace pmpe {
 namespace {
 
-constexpr int RT_TOK = 32;
-constexpr int RT_WAVES = 8;
+constexpr int RT_WAVES = 4;
 constexpr int RT_THREADS = 64 * RT_WAVES;
 
 // Descending sort key of an fp32 logit: smaller key = larger logit.
@@ -81,6 +80,17 @@ __device__ __forceinline__ void wave_bitonic_sort(uint64_t (&v)[NPL]) {
       }
     }
   }
+}
+
+// tau of token t: only the exact allow word allows; with no private router the token
+// fails closed to deny (and the status bit is raised).
+__device__ __forceinline__ int token_tau(const RouteArgs& a, int t) {
+  int tau = (a.words != nullptr && a.words[t] == PMPE_POLICY_ALLOW) ? 1 : 0;
+  if (tau == 1 && a.wr_priv == nullptr) {
+    tau = 0;
+    if (a.dev_status) atomicOr(a.dev_status, PMPE_DEV_PRIV_ROUTER_MISSING);
+  }
+  return tau;
 }
 
 struct TopkCtx {
@@ -144,138 +154,162 @@ __device__ void topk_one_token(const TopkCtx& c, int t, int tau, const float* z)
   }
 }
 
-template <bool ACT_BF16>
-__global__ __launch_bounds__(RT_THREADS) void route_kernel(RouteArgs a) {
-  __shared__ int s_tau[RT_TOK];
-  __shared__ int s_need[2];
-  __shared__ float s_z[RT_TOK][PMPE_MAX_POOL];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int t0 = blockIdx.x * RT_TOK;
-
-  if (tid < 2) s_need[tid] = 0;
+// Token-tile x expert-group logits. Block (tile, g): TT tokens against 16 experts of
+// one pool; the four waves split H in quarters (each wave starts its quarter at a
+// block-dependent step so that concurrent blocks read different router columns) and
+// their partial sums are added in fixed wave order, then the bias. Only tokens whose
+// policy selects this pool are fed (others are zero rows) and written.
+template <int TT>
+__global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs a) {
+  constexpr int NMB = TT / 16;
+  __shared__ int s_tau[TT];
+  __shared__ int s_any;
+  __shared__ float s_part[RT_WAVES][TT][16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t0 = blockIdx.x * TT;
+  const int gpub = (a.n_pub + 15) >> 4;
+  const int pass = blockIdx.y < gpub ? 0 : 1;
+  const int n0 = (pass ? blockIdx.y - gpub : blockIdx.y) * 16;
+  const int N = pass ? a.n_priv : a.n_pub;
+  if (tid == 0) s_any = 0;
   __syncthreads();
-  if (tid < RT_TOK) {
-    const int t = t0 + tid;
-    int tau = -1;
-    if (t < a.T) {
-      tau = (a.words != nullptr && a.words[t] == PMPE_POLICY_ALLOW) ? 1 : 0;
-      if (tau == 1 && a.wr_priv == nullptr) {
-        tau = 0;  // fail closed: no private router, the row is routed as deny
-        if (a.dev_status) atomicOr(a.dev_status, PMPE_DEV_PRIV_ROUTER_MISSING);
-      }
-      s_need[tau] = 1;
-    }
+  if (tid < TT) {
+    const int tau = (t0 + tid < a.T) ? token_tau(a, t0 + tid) : -1;
     s_tau[tid] = tau;
+    if (tau == pass) s_any = 1;
   }
   __syncthreads();
-
-  for (int pass = 0; pass < 2; ++pass) {
-    if (!s_need[pass]) continue;  // uniform: no token of this policy in the tile
-    const float* wr = pass ? a.wr_priv : a.wr_pub;
-    const int N = pass ? a.n_priv : a.n_pub;
-    const int bias_base = pass ? a.n_pub : 0;
-    const int H = a.H;
-    if constexpr (ACT_BF16) {
-      const uint16_t* x = (const uint16_t*)a.x;
-      const int nblk = (N + 15) >> 4;
-      for (int j = wave; j < nblk; j += RT_WAVES) {
-        const int n = (j << 4) + (lane & 15);
-        const bool nv = n < N;
-        const int koff = (lane >> 4) * 8;
-        const float* wrow = wr + (size_t)(nv ? n : 0) * H + koff;
-        bool av[2];
-        const uint16_t* xrow[2];
+  if (!s_any) return;  // no token of this pool's policy in the tile: rows never read
+  const float* wr = pass ? a.wr_priv : a.wr_pub;
+  const int H = a.H;
+  const uint16_t* x = (const uint16_t*)a.x;
+  const int n = n0 + (lane & 15);
+  const bool nv = n < N;
+  const int koff = (lane >> 4) * 8;
+  const float* wrow = wr + (size_t)(nv ? n : n0) * H + koff;
+  const uint16_t* xrow[NMB];
+  bool av[NMB];
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-          const int tt = mb * 16 + (lane & 15);
-          av[mb] = s_tau[tt] == pass;
-          xrow[mb] = x + (size_t)(av[mb] ? t0 + tt : 0) * H + koff;
-        }
-        f32x4 acc[2] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
-#pragma unroll 4
-        for (int kk = 0; kk < H; kk += 32) {
-          float4 w0 = make_float4(0, 0, 0, 0), w1 = w0;
-          if (nv) {
-            w0 = *(const float4*)(wrow + kk);
-            w1 = *(const float4*)(wrow + kk + 4);
-          }
-          u32x4 xa[2];
+  for (int mb = 0; mb < NMB; ++mb) {
+    const int tt = mb * 16 + (lane & 15);
+    av[mb] = s_tau[tt] == pass;
+    xrow[mb] = x + (size_t)(av[mb] ? t0 + tt : t0) * H + koff;
+  }
+  const int nsteps = H / (32 * RT_WAVES);  // K steps of this wave's quarter
+  const int kbase = wave * nsteps;
+  const int rot = (blockIdx.x * 5 + blockIdx.y * 3) % nsteps;
+  f32x4 acc[NMB];
 #pragma unroll
-          for (int mb = 0; mb < 2; ++mb) {
-            xa[mb] = av[mb] ? *(const u32x4*)(xrow[mb] + kk) : u32x4{0, 0, 0, 0};
-          }
-          const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-          uint32_t ph[8], pm[8], pl[8];
+  for (int mb = 0; mb < NMB; ++mb) acc[mb] = f32x4{0, 0, 0, 0};
+  constexpr int D = 4;  // K steps per batch of loads in flight
+  for (int s0 = 0; s0 < nsteps; s0 += D) {
+    float4 w[D][2];
+    u32x4 xa[D][NMB];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
-          const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
-                                            ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
-          const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
-                                            pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
-          const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
-                                            pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
-#pragma unroll
-          for (int mb = 0; mb < 2; ++mb) {
-            const bf16x8 av8 = as_bf16x8(xa[mb]);
-            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[mb], 0, 0, 0);
-            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[mb], 0, 0, 0);
-            acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[mb], 0, 0, 0);
-          }
-        }
-        const float b = (nv && a.bias) ? a.bias[bias_base + n] : 0.0f;
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int tt = mb * 16 + (lane >> 4) * 4 + i;
-            if (nv && s_tau[tt] == pass) s_z[tt][n] = a.bias ? acc[mb][i] + b : acc[mb][i];
-          }
-        }
+    for (int d = 0; d < D; ++d) {
+      int st = s0 + d;
+      const bool sv = st < nsteps;
+      st = (st + rot) % nsteps;
+      const int kk = (kbase + st) * 32;
+      w[d][0] = make_float4(0, 0, 0, 0);
+      w[d][1] = w[d][0];
+      if (sv && nv) {
+        w[d][0] = *(const float4*)(wrow + kk);
+        w[d][1] = *(const float4*)(wrow + kk + 4);
       }
-    } else {
-      const float* x = (const float*)a.x;
-      for (int p = tid; p < RT_TOK * N; p += RT_THREADS) {
-        const int tt = p / N, n = p - tt * N;
-        if (s_tau[tt] != pass) continue;
-        const float* xr = x + (size_t)(t0 + tt) * H;
-        const float* wrow = wr + (size_t)n * H;
-        float acc = 0.0f;
-        for (int h0 = 0; h0 < H; h0 += 64) {  // blocked: partial sums of 64 terms
-          float part = 0.0f;
-          for (int h = h0; h < h0 + 64; ++h) part = fmaf(xr[h], wrow[h], part);
-          acc += part;
-        }
-        s_z[tt][n] = a.bias ? acc + a.bias[bias_base + n] : acc;
+#pragma unroll
+      for (int mb = 0; mb < NMB; ++mb)
+        xa[d][mb] = (sv && av[mb]) ? *(const u32x4*)(xrow[mb] + kk) : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const float wv[8] = {w[d][0].x, w[d][0].y, w[d][0].z, w[d][0].w,
+                           w[d][1].x, w[d][1].y, w[d][1].z, w[d][1].w};
+      uint32_t ph[8], pm[8], pl[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
+      const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
+                                        ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
+      const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
+                                        pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
+      const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
+                                        pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
+#pragma unroll
+      for (int mb = 0; mb < NMB; ++mb) {
+        const bf16x8 av8 = as_bf16x8(xa[d][mb]);
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[mb], 0, 0, 0);
       }
     }
   }
+#pragma unroll
+  for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s_part[wave][mb * 16 + (lane >> 4) * 4 + i][lane & 15] = acc[mb][i];
   __syncthreads();
-
-  TopkCtx c{a.T, a.n_pub, a.n_priv, a.k, a.gate_mode, a.topk_idx, a.topk_gate, a.allow, a.kgap};
-  for (int tt = wave; tt < RT_TOK; tt += RT_WAVES) {
-    const int tau = s_tau[tt];
-    if (tau < 0) continue;
-    const int N = tau ? a.n_priv : a.n_pub;
-    if (N <= 64)
-      topk_one_token<1>(c, t0 + tt, tau, s_z[tt]);
-    else if (N <= 128)
-      topk_one_token<2>(c, t0 + tt, tau, s_z[tt]);
-    else
-      topk_one_token<4>(c, t0 + tt, tau, s_z[tt]);
+  for (int o = tid; o < TT * 16; o += RT_THREADS) {
+    const int tt = o >> 4, c = o & 15;
+    const int nn = n0 + c;
+    if (s_tau[tt] != pass || nn >= N) continue;
+    float z = s_part[0][tt][c];
+#pragma unroll
+    for (int w2 = 1; w2 < RT_WAVES; ++w2) z += s_part[w2][tt][c];
+    if (a.bias) z += a.bias[(pass ? a.n_pub : 0) + nn];
+    a.z[(size_t)(t0 + tt) * a.zstride + nn] = z;
   }
+}
+
+// fp32 activations (small layers): one thread per (token, expert) pair, fp32 dot
+// products in blocks of 64 terms.
+__global__ __launch_bounds__(RT_THREADS) void route_logits_f32_kernel(RouteArgs a) {
+  const int t = blockIdx.x;
+  const int tau = token_tau(a, t);
+  const int N = tau ? a.n_priv : a.n_pub;
+  const float* wr = tau ? a.wr_priv : a.wr_pub;
+  const float* xr = (const float*)a.x + (size_t)t * a.H;
+  for (int n = threadIdx.x; n < N; n += RT_THREADS) {
+    const float* wrow = wr + (size_t)n * a.H;
+    float acc = 0.0f;
+    for (int h0 = 0; h0 < a.H; h0 += 64) {
+      float part = 0.0f;
+      for (int h = h0; h < h0 + 64; ++h) part = fmaf(xr[h], wrow[h], part);
+      acc += part;
+    }
+    if (a.bias) acc += a.bias[(tau ? a.n_pub : 0) + n];
+    a.z[(size_t)t * a.zstride + n] = acc;
+  }
+}
+
+// Top-k and gates: one wave per token over its pool's logits.
+__global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
+  const int t = blockIdx.x * RT_WAVES + (threadIdx.x >> 6);
+  if (t >= a.T) return;
+  const int tau = token_tau(a, t);
+  const int N = tau ? a.n_priv : a.n_pub;
+  const float* z = a.z + (size_t)t * a.zstride;
+  TopkCtx c{a.T, a.n_pub, a.n_priv, a.k, a.gate_mode, a.topk_idx, a.topk_gate, a.allow, a.kgap};
+  if (N <= 64)
+    topk_one_token<1>(c, t, tau, z);
+  else if (N <= 128)
+    topk_one_token<2>(c, t, tau, z);
+  else
+    topk_one_token<4>(c, t, tau, z);
 }
 
 }  // namespace
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
-  const dim3 grid((a.T + RT_TOK - 1) / RT_TOK), block(RT_THREADS);
-  if (a.act_bf16)
-    hipLaunchKernelGGL(route_kernel<true>, grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL(route_kernel<false>, grid, block, 0, s, a);
+  if (a.act_bf16) {
+    const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
+    if (a.T > 2048)
+      hipLaunchKernelGGL(route_logits_bf16_kernel<32>, dim3((a.T + 31) / 32, groups), dim3(RT_THREADS), 0, s, a);
+    else
+      hipLaunchKernelGGL(route_logits_bf16_kernel<16>, dim3((a.T + 15) / 16, groups), dim3(RT_THREADS), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(route_logits_f32_kernel, dim3(a.T), dim3(RT_THREADS), 0, s, a);
+  }
+  hipLaunchKernelGGL(route_topk_kernel, dim3((a.T + RT_WAVES - 1) / RT_WAVES), dim3(RT_THREADS), 0, s, a);
   return hipGetLastError();
 }
 

@@ -102,7 +102,7 @@ class PolicyMaskedMoE:
     def route(self, x, words, b: LayerBuffers, stream=None):
         T = x.shape[0]
         N.pmpe_route(self.desc, T, x, self.wr_pub, self.wr_priv, self.bias, words, b.topk_idx,
-                     b.topk_gate, b.allow, b.kgap, b.dev_status, stream)
+                     b.topk_gate, b.allow, b.kgap, b.dev_status, b.ws, stream)
 
     def dispatch(self, x, b: LayerBuffers, stream=None):
         T = x.shape[0]

@@ -98,11 +98,15 @@ def test_null_and_alignment_rejected_before_launch():
     lib = N.lib()
     # NULL x
     st = lib.pmpe_route(ctypes.byref(d), 16, None, 0x1000, None, None, None, 0x2000, 0x3000, 0x4000,
-                        None, None, None)
+                        None, None, 0x5000, 1 << 20, None)
     assert st == -1
+    # route without workspace
+    st = lib.pmpe_route(ctypes.byref(d), 16, 0x1000, 0x1000, None, None, None, 0x2000, 0x3000,
+                        0x4000, None, None, None, 0, None)
+    assert st == -6
     # misaligned x
     st = lib.pmpe_route(ctypes.byref(d), 16, 0x1004, 0x1000, None, None, None, 0x2000, 0x3000,
-                        0x4000, None, None, None)
+                        0x4000, None, None, 0x5000, 1 << 20, None)
     assert st == -5
     # dispatch without workspace
     st = lib.pmpe_dispatch(ctypes.byref(d), 16, 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000,
@@ -126,7 +130,7 @@ def test_zero_tokens_launch_nothing():
     d = desc()
     lib = N.lib()
     assert lib.pmpe_route(ctypes.byref(d), 0, 0x1000, 0x1000, None, None, None, 0x2000, 0x3000,
-                          0x4000, None, None, None) == 0
+                          0x4000, None, None, None, 0, None) == 0
     assert lib.pmpe_combine(ctypes.byref(d), 0, 0x1000, 0x2000, 0x3000, None, 0x4000, None) == 0
 
 
