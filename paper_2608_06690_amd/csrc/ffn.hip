@@ -26,6 +26,8 @@
 // row (their results are never stored), and MFMAs of 16-row blocks that hold no
 // valid row are skipped. The output tile goes through LDS so that global stores are
 // whole 16-byte vectors.
+#include <type_traits>
+
 #include "pmpe_internal.h"
 
 namespace pmpe {
@@ -51,6 +53,31 @@ __device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
       "s"(lds_base)
       : "memory", "m0");
 }
+// Same copy addressed as a wave-uniform 64-bit base (SGPRs) plus a per-lane 32-bit
+// byte offset; the LDS destination is a wave-uniform base plus the immediate IMM.
+template <int IMM>
+__device__ __forceinline__ void dma16s(uint32_t byte_off, const void* base, uint32_t lds_base) {
+  asm volatile(
+      "s_add_u32 m0, %2, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1 offset:0" ::"v"(byte_off),
+      "s"(base), "s"(lds_base), "n"(IMM)
+      : "memory", "m0");
+}
+
+template <int I, int N>
+struct Unroll {
+  template <class F>
+  __device__ __forceinline__ static void run(F&& f) {
+    f(std::integral_constant<int, I>{});
+    Unroll<I + 1, N>::run(f);
+  }
+};
+template <int N>
+struct Unroll<N, N> {
+  template <class F>
+  __device__ __forceinline__ static void run(F&&) {}
+};
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -75,15 +102,19 @@ __device__ __forceinline__ int swz(int r, int c) {
     return r * 64 + ((c ^ ((r >> 1) & 3)) << 4);
 }
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_, int FRAG_BUFS_ = 1>
 struct Cfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, BK = BK_;
+  static constexpr int FRAG_BUFS = FRAG_BUFS_;  // 2: read the next K step's fragments early
   static constexpr int RB = 2 * BK, CH = BK / 8, RPD = 1024 / RB;  // rows per DMA instruction
   static constexpr int WAVES = WM * WN, THREADS = 64 * WAVES;
   static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB, STAGE = A_BYTES + B_BYTES;
   static constexpr int A_DMA = BM / RPD / WAVES, B_DMA = BN / RPD / WAVES;  // per wave per stage
+  // A wave owns MB 16-row blocks of the tile, interleaved with the other WM-1 row
+  // waves (block j*WM + wm), so a partly filled tile loads every SIMD evenly.
   static constexpr int WROWS = BM / WM, MB = WROWS / 16;
   static constexpr int LDS = STAGES * STAGE;
+  static constexpr int PER_CU = (160 * 1024 - 8 * 1024) / LDS;  // resident blocks per CU
   static_assert(BK == 32 || BK == 64, "BK");
   static_assert(A_DMA * RPD * WAVES == BM && B_DMA * RPD * WAVES == BN, "DMA split");
 };
@@ -91,24 +122,65 @@ struct Cfg {
 #define PMPE_CFG_LARGE 256, 256, 4, 2, 2, 64
 #endif
 #ifndef PMPE_CFG_SMALL
-#define PMPE_CFG_SMALL 64, 128, 1, 4, 3, 64
+#define PMPE_CFG_SMALL 64, 128, 1, 4, 3, 64, 2
 #endif
-using CfgLarge = Cfg<PMPE_CFG_LARGE>;  // prefill: 8 waves, 2 x 64 KiB stages
+using CfgLarge = Cfg<PMPE_CFG_LARGE>;  // prefill: 8 waves of 64 x 128, 2 x 64 KiB stages
 using CfgSmall = Cfg<PMPE_CFG_SMALL>;  // decode-shaped: 4 waves, 3 x 24 KiB stages
 
-struct GTile {
-  int g;     // group: expert id, or E for the shared group; -1: no tile
+constexpr int MAXG = 2 * PMPE_MAX_POOL + 1;  // routed experts + the shared group
+
+// DMA of 4 bytes per lane (int32 gather indices): lane l's word lands at lds_base + 4 * l.
+__device__ __forceinline__ void dma4(const void* src, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %0, off" ::"v"(src),
+      "s"(lds_base)
+      : "memory", "m0");
+}
+
+struct TileInfo {
+  int g;     // group: expert id, or E for the shared group
   int m0;    // first row of the tile within the group
   int n0;    // first output column (GEMM1: h column; GEMM2: y column)
   int rows;  // valid rows
   int base;  // first row of the tile in the group's row space (permuted row / token)
 };
 
-// Block-uniform tile lookup. ncols = output columns per N tile.
-__device__ GTile lookup_tile(const FfnArgs& a, bool gemm1, int BMv, int ncols, int* s_cum) {
+// Persistent bf16 grouped GEMM. GATED: GEMM1 (x -> h with SwiGLU); else GEMM2 (h -> y).
+//
+// Each block builds the group table once (tile counts, row counts and offsets in LDS),
+// then walks its share of the tile list: XCD x = blockIdx % 8 owns a contiguous slice
+// of the (group, N tile, M tile) order, dealt round-robin to the XCD's blocks. K steps
+// of consecutive tiles form one stream: the copy ring keeps STAGES-1 steps in flight
+// across tile boundaries, so the next tile's first operands load during the current
+// tile's last MFMAs and its epilogue. Gather indices (row_token slices) are fetched by
+// LDS-DMA as well, one tile ahead of their use, so no register-destined global load
+// inside the stream forces the compiler to drain the ring.
+template <class C, bool GATED>
+__global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
+  __shared__ __attribute__((aligned(16))) int s_rt[3][C::BM];
+  __shared__ int s_cum[MAXG + 1];
+  __shared__ int s_cnt[MAXG];
+  __shared__ int s_off[MAXG];
+  constexpr int NCOLS = GATED ? C::BN / 2 : C::BN;  // output columns per tile
+  constexpr int WCOLS = NCOLS / C::WN;               // output columns per wave
+  constexpr int NBO = WCOLS / 16;                    // output 16-col blocks per wave
+  constexpr int NB = GATED ? 2 * NBO : NBO;          // B operand blocks per wave
+  constexpr int BK = C::BK, S = C::STAGES, NDMA = C::A_DMA + C::B_DMA;
+  constexpr int ER = (C::STAGE / (NCOLS * 2)) < C::BM ? (C::STAGE / (NCOLS * 2)) : C::BM;  // epilogue rows per pass
+  static_assert(ER % 16 == 0 && C::BM % ER == 0, "an epilogue pass must hold whole 16-row blocks");
+  static_assert(C::BM % 64 == 0 || C::BM <= 64, "row_token slice copy");
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int uwave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, scalar
+  const int wm = uwave / C::WN, wn = uwave % C::WN;
   const int E = a.n_pub + a.n_priv;
   const int ngroups = E + (a.Is > 0 ? 1 : 0);
-  const int tid = threadIdx.x;
+  const int H = a.H;
+  const int TK = a.T * a.k;
+
   if (tid < 64) {
     int running = 0;
     for (int g0 = 0; g0 < ngroups; g0 += 64) {
@@ -116,8 +188,10 @@ __device__ GTile lookup_tile(const FfnArgs& a, bool gemm1, int BMv, int ncols, i
       int nt = 0;
       if (g < ngroups) {
         const int cnt = (g < E) ? a.count[g] : a.T;
-        const int width = gemm1 ? ((g < E) ? a.I : a.Is) : a.H;
-        nt = ((cnt + BMv - 1) / BMv) * ((width + ncols - 1) / ncols);
+        s_cnt[g] = cnt;
+        s_off[g] = (g < E) ? a.offset[g] : 0;
+        const int width = GATED ? ((g < E) ? a.I : a.Is) : H;
+        nt = ((cnt + C::BM - 1) / C::BM) * ((width + NCOLS - 1) / NCOLS);
       }
       const int incl = wave_incl_scan(nt);
       if (g < ngroups) s_cum[g + 1] = running + incl;
@@ -126,131 +200,151 @@ __device__ GTile lookup_tile(const FfnArgs& a, bool gemm1, int BMv, int ncols, i
     if (tid == 0) s_cum[0] = 0;
   }
   __syncthreads();
-  GTile t;
-  t.g = -1;
+
+  // This block's tiles: L_i = start_x + q + i * nbx, i < ntl.
   const int total = s_cum[ngroups];
-  const int b = blockIdx.x;
-  if (b >= total) return t;
-  // XCD-aware order: XCD x = b % 8 takes a contiguous range of the tile order
-  const int x = b & 7, j = b >> 3;
-  const int L = x * (total >> 3) + min(x, total & 7) + j;
-  int lo = 0, hi = ngroups - 1;  // last g with s_cum[g] <= L
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (s_cum[mid] <= L) lo = mid; else hi = mid - 1;
-  }
-  const int g = lo;
-  const int cnt = (g < E) ? a.count[g] : a.T;
-  const int mt = (cnt + BMv - 1) / BMv;
-  const int local = L - s_cum[g];
-  const int n = local / mt, m = local - n * mt;
-  t.g = g;
-  t.m0 = m * BMv;
-  t.n0 = n * ncols;
-  t.rows = min(BMv, cnt - t.m0);
-  t.base = ((g < E) ? a.offset[g] : 0) + t.m0;
-  return t;
-}
+  const int b = blockIdx.x, x = b & 7, q = b >> 3;
+  const int nbx = ((int)gridDim.x - x + 7) >> 3;
+  const int cnt_x = (total >> 3) + (x < (total & 7) ? 1 : 0);
+  const int start_x = x * (total >> 3) + min(x, total & 7);
+  const int ntl = (cnt_x > q) ? (cnt_x - q + nbx - 1) / nbx : 0;
+  if (ntl == 0) return;
 
-// One bf16 GEMM tile. GATED: GEMM1 (x -> h with SwiGLU); else GEMM2 (h -> y).
-template <class C, bool GATED>
-__global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
-  __shared__ int s_cum[2 * PMPE_MAX_POOL + 2];
-  constexpr int NCOLS = GATED ? C::BN / 2 : C::BN;  // output columns per tile
-  constexpr int WCOLS = NCOLS / C::WN;               // output columns per wave
-  constexpr int NBO = WCOLS / 16;                    // output 16-col blocks per wave
-  constexpr int NB = GATED ? 2 * NBO : NBO;          // B operand blocks per wave
-  static_assert(C::BM * NCOLS * 2 <= C::LDS, "output tile must fit the LDS ring");
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / C::WN, wn = wave % C::WN;
-  const int E = a.n_pub + a.n_priv;
-
-  const GTile t = lookup_tile(a, GATED, C::BM, NCOLS, s_cum);
-  if (t.g < 0) return;
-  const bool shared = t.g >= E;
-  const bool priv = !shared && t.g >= a.n_pub;
-  const int I = shared ? a.Is : a.I;
-  const int H = a.H;
-  const int K = GATED ? H : I;
-  const int width = GATED ? I : H;  // valid output columns
-
-  const uint16_t* w;
-  if (shared) {
-    w = (const uint16_t*)(GATED ? a.w13_sh : a.w2_sh);
-  } else if (!priv) {
-    w = (const uint16_t*)(GATED ? a.w13_pub : a.w2_pub) + (size_t)t.g * 2 * I * H / (GATED ? 1 : 2);
-  } else {
-    if (a.w13_priv == nullptr || a.w2_priv == nullptr) {
-      if (!GATED) {
-        // private rows without private weights: not executed, not audited, y zeroed
-        if (tid == 0 && a.dev_status) atomicOr(a.dev_status, PMPE_DEV_PRIV_WEIGHTS_MISSING);
-        uint16_t* y = (uint16_t*)a.y_perm;
-        for (int i = tid; i < t.rows * NCOLS; i += C::THREADS) {
-          const int r = i / NCOLS, c = t.n0 + i % NCOLS;
-          if (c < width) y[(size_t)(t.base + r) * H + c] = 0;
-        }
-      }
-      return;
+  auto tile_of = [&](int i) {
+    const int L = start_x + q + i * nbx;
+    int lo = 0, hi = ngroups - 1;  // last g with s_cum[g] <= L (a group with tiles)
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_cum[mid] <= L) lo = mid; else hi = mid - 1;
     }
-    w = (const uint16_t*)(GATED ? a.w13_priv : a.w2_priv) +
-        (size_t)(t.g - a.n_pub) * 2 * I * H / (GATED ? 1 : 2);
-  }
-
-  // Per-lane source rows of this wave's DMA instructions. DMA instruction i of wave
-  // `wave` fills the RPD operand rows r0 = (wave * n + i) * RPD ..; lane l writes LDS
-  // chunk (row r0 + l / CH, physical chunk l % CH), which holds the logical chunk whose
-  // swizzled position that is.
-  constexpr int BK = C::BK;
-  const int lrow = lane / C::CH, lphys = lane % C::CH;
-  auto logical = [&](int r) { return (BK == 64) ? (lphys ^ (r & 7)) : (lphys ^ ((r >> 1) & 3)); };
-  const uint16_t* srcA[C::A_DMA];
-  const uint16_t* srcB[C::B_DMA];
-#pragma unroll
-  for (int i = 0; i < C::A_DMA; ++i) {
-    const int r = (wave * C::A_DMA + i) * C::RPD + lrow;
-    const int rr = min(r, t.rows - 1);  // rows past the valid count reload a valid row
-    const int c = logical(r);
-    const uint16_t* row;
-    if (GATED) {
-      if (shared)
-        row = (const uint16_t*)a.x + (size_t)(t.base + rr) * H;
-      else if (a.x_perm)
-        row = (const uint16_t*)a.x_perm + (size_t)(t.base + rr) * H;
-      else
-        row = (const uint16_t*)a.x + (size_t)a.row_token[t.base + rr] * H;
-    } else {
-      row = (const uint16_t*)(shared ? a.h_sh : a.h) + (size_t)(t.base + rr) * I;
-    }
-    srcA[i] = row + c * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < C::B_DMA; ++i) {
-    const int r = (wave * C::B_DMA + i) * C::RPD + lrow;
-    const int c = logical(r);
-    int wrow;
-    if (GATED) {
-      const int half = C::BN / 2;
-      const int j = (r < half) ? r : r - half;
-      const int col = min(t.n0 + j, I - 1);
-      wrow = (r < half) ? col : I + col;
-    } else {
-      wrow = min(t.n0 + r, H - 1);
-    }
-    srcB[i] = w + (size_t)wrow * K + c * 8;
-  }
-
-  const uint32_t lds0 = lds_addr(smem);
-  const int uwave = __builtin_amdgcn_readfirstlane(wave);  // wave index as a scalar
-  auto issue = [&](int stage, int k0) {
-    const uint32_t sa = lds0 + stage * C::STAGE;
-    const uint32_t sb = sa + C::A_BYTES;
-#pragma unroll
-    for (int i = 0; i < C::A_DMA; ++i) dma16(srcA[i] + k0, sa + (uwave * C::A_DMA + i) * 1024);
-#pragma unroll
-    for (int i = 0; i < C::B_DMA; ++i) dma16(srcB[i] + k0, sb + (uwave * C::B_DMA + i) * 1024);
+    TileInfo t;
+    t.g = __builtin_amdgcn_readfirstlane(lo);
+    const int cnt = __builtin_amdgcn_readfirstlane(s_cnt[t.g]);
+    const int mt = (cnt + C::BM - 1) / C::BM;
+    const int local = L - __builtin_amdgcn_readfirstlane(s_cum[t.g]);
+    const int n = local / mt, m = local - n * mt;
+    t.m0 = m * C::BM;
+    t.n0 = n * NCOLS;
+    t.rows = min(C::BM, cnt - t.m0);
+    t.base = __builtin_amdgcn_readfirstlane(s_off[t.g]) + t.m0;
+    return t;
   };
+  // Does tile t read row_token? (gathered x rows in GEMM1; the audit in GEMM2)
+  auto needs_rt = [&](const TileInfo& t) {
+    if (t.g >= E) return false;
+    return GATED ? (a.x_perm == nullptr) : (t.g >= a.n_pub);
+  };
+  const uint32_t lds0 = lds_addr(smem);
+  const uint32_t rt0 = lds_addr(&s_rt[0][0]);
+  // Copy row_token[base .. base + BM) of tile t into s_rt[slot] (wave 0; clamped reads).
+  auto issue_rt = [&](const TileInfo& t, int slot) {
+    if (uwave == 0 && needs_rt(t)) {
+#pragma unroll
+      for (int j = 0; j < (C::BM + 63) / 64; ++j) {
+        const int idx = min(t.base + j * 64 + lane, TK - 1);
+        dma4(a.row_token + idx, rt0 + (slot * C::BM + j * 64) * 4);
+      }
+    }
+  };
+
+  // Producer context: source pointers of the tile whose K steps are being issued.
+  constexpr int CHK = C::CH;
+  const int lrow = lane / CHK, lphys = lane % CHK;
+  auto logical = [&](int r) { return (BK == 64) ? (lphys ^ (r & 7)) : (lphys ^ ((r >> 1) & 3)); };
+  // Copy sources as 32-bit element offsets from tile-uniform bases (the host checks
+  // that every offset fits).
+  uint32_t offA[C::A_DMA], offB[C::B_DMA];
+  const uint16_t* baseA = nullptr;
+  const uint16_t* baseB = nullptr;
+  bool p_valid = true;  // producer tile has weights (private tiles may not)
+  auto setup_ctx = [&](const TileInfo& t, int slot) {
+    const bool shared = t.g >= E;
+    const bool priv = !shared && t.g >= a.n_pub;
+    const int I = shared ? a.Is : a.I;
+    const int K = GATED ? H : I;
+    const uint16_t* w;
+    if (shared) {
+      w = (const uint16_t*)(GATED ? a.w13_sh : a.w2_sh);
+    } else if (!priv) {
+      w = (const uint16_t*)(GATED ? a.w13_pub : a.w2_pub) + (size_t)t.g * (GATED ? 2 : 1) * I * H;
+    } else {
+      w = (const uint16_t*)(GATED ? a.w13_priv : a.w2_priv);
+      if (w) w += (size_t)(t.g - a.n_pub) * (GATED ? 2 : 1) * I * H;
+    }
+    p_valid = (w != nullptr) && !(priv && (a.w13_priv == nullptr || a.w2_priv == nullptr));
+    if (!p_valid) w = (const uint16_t*)(GATED ? a.w13_pub : a.w2_pub);  // read but never used
+    if (GATED)
+      baseA = (const uint16_t*)((!shared && a.x_perm) ? a.x_perm : a.x);
+    else
+      baseA = (const uint16_t*)(shared ? a.h_sh : a.h);
+    baseB = w;
+#pragma unroll
+    for (int i = 0; i < C::A_DMA; ++i) {
+      const int r = (uwave * C::A_DMA + i) * C::RPD + lrow;
+      const int rr = min(r, t.rows - 1);  // rows past the valid count reload a valid row
+      uint32_t row;
+      if (GATED) {
+        if (shared || a.x_perm)
+          row = (uint32_t)(t.base + rr) * (uint32_t)H;
+        else
+          row = (uint32_t)s_rt[slot][rr] * (uint32_t)H;
+      } else {
+        row = (uint32_t)(t.base + rr) * (uint32_t)I;
+      }
+      offA[i] = (row + logical(r) * 8) * 2;  // bytes
+    }
+#pragma unroll
+    for (int i = 0; i < C::B_DMA; ++i) {
+      const int r = (uwave * C::B_DMA + i) * C::RPD + lrow;
+      int wrow;
+      if (GATED) {
+        const int half = C::BN / 2;
+        const int j = (r < half) ? r : r - half;
+        const int col = min(t.n0 + j, I - 1);
+        wrow = (r < half) ? col : I + col;
+      } else {
+        wrow = min(t.n0 + r, H - 1);
+      }
+      offB[i] = ((uint32_t)wrow * (uint32_t)K + logical(r) * 8) * 2;  // bytes
+    }
+    return K / BK;
+  };
+  auto issue = [&](int slot, int k0) {
+    const uint32_t sa = lds0 + slot * C::STAGE;
+    const uint32_t sb = sa + C::A_BYTES;
+    const uint16_t* ba = baseA + k0;  // scalar bases advance by the K step
+    const uint16_t* bb = baseB + k0;
+    const uint32_t wa = sa + uwave * C::A_DMA * 1024, wb = sb + uwave * C::B_DMA * 1024;
+    Unroll<0, C::A_DMA>::run([&](auto i) { dma16s<i.value * 1024>(offA[i.value], ba, wa); });
+    Unroll<0, C::B_DMA>::run([&](auto i) { dma16s<i.value * 1024>(offB[i.value], bb, wb); });
+  };
+
+  // Producer state: next step to issue is (pi, pk) of a tile with pnk steps; `issued`
+  // counts the steps issued so far.
+  int pi = 0, pk = 0, pnk = 0, issued = 0;
+  TileInfo pt = tile_of(0);
+  // prologue: gather indices of tiles 0 and 1, then the first S-1 steps
+  issue_rt(pt, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  pnk = setup_ctx(pt, 0);
+  if (ntl > 1) issue_rt(tile_of(1), 1);
+  auto produce = [&](int slot) {  // issue the next step into `slot` (if any remain)
+    if (pi >= ntl) return;
+    if (pk == pnk) {  // advance to the next tile; its gather indices arrived earlier
+      ++pi;
+      pk = 0;
+      if (pi >= ntl) return;
+      pt = tile_of(pi);
+      pnk = setup_ctx(pt, pi % 3);
+      if (pi + 1 < ntl) issue_rt(tile_of(pi + 1), (pi + 1) % 3);
+    }
+    issue(slot, pk * BK);
+    ++pk;
+    ++issued;
+  };
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s) produce(s);
 
   f32x4 acc[C::MB][NB];
 #pragma unroll
@@ -258,106 +352,140 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0, 0, 0, 0};
 
-  // 16-row blocks of this wave that hold at least one valid row
-  const int wrow0 = wm * C::WROWS;
-  const int mb_live = max(0, min(C::MB, (t.rows - wrow0 + 15) / 16));
-
-  // B operand row (within the tile) of this wave's block nb, for lane row l16
-  auto brow = [&](int nb) {
-    if (GATED) {
-      const int half = C::BN / 2;
-      return (nb < NBO) ? wn * WCOLS + nb * 16 : half + wn * WCOLS + (nb - NBO) * 16;
-    }
-    return wn * WCOLS + nb * 16;
+  // B operand row (within the tile) of block nb of this wave, minus the wave's offset
+  auto bconst = [&](int nb) {
+    if (GATED) return (nb < NBO) ? nb * 16 : C::BN / 2 + (nb - NBO) * 16;
+    return nb * 16;
   };
-
-  const int nk = K / BK;
+  constexpr int SUB = BK / 32;
+  constexpr int FB = C::FRAG_BUFS;
+  bf16x8 fa[FB][C::MB], fb[FB][NB];
+  // Every operand block starts at a multiple of 16 rows, so the swizzled position of a
+  // lane's chunk depends on the lane alone: one per-lane offset per K sub-step, plus a
+  // wave-uniform part, plus a compile-time part that fits the ds_read offset field.
+  uint32_t lane_off[SUB];
 #pragma unroll
-  for (int s = 0; s < C::STAGES - 1; ++s)
-    if (s < nk) issue(s, s * BK);
-
-  constexpr int SUB = BK / 32;  // MFMA K steps per stage
-  bf16x8 fa[2][C::MB], fb[2][NB];
-  auto read_frags = [&](const unsigned char* sa, const unsigned char* sb, int sub, int buf) {
-    const int ch = sub * 4 + (lane >> 4);
+  for (int sub = 0; sub < SUB; ++sub) lane_off[sub] = (uint32_t)swz<BK>(lane & 15, sub * 4 + (lane >> 4));
+  auto read_frags = [&](int slot, int sub, int buf) {
+    const uint32_t pa = lane_off[sub] + slot * C::STAGE + wm * 16 * C::RB;
+    const uint32_t pb = lane_off[sub] + slot * C::STAGE + C::A_BYTES + wn * WCOLS * C::RB;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      fb[buf][nb] = as_bf16x8(*(const u32x4*)(sb + swz<BK>(brow(nb) + (lane & 15), ch)));
+    for (int nb = 0; nb < NB; ++nb) fb[buf][nb] = as_bf16x8(*(const u32x4*)(smem + pb + bconst(nb) * C::RB));
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb)
-      fa[buf][mb] = as_bf16x8(*(const u32x4*)(sa + swz<BK>(wrow0 + mb * 16 + (lane & 15), ch)));
+      fa[buf][mb] = as_bf16x8(*(const u32x4*)(smem + pa + mb * C::WM * 16 * C::RB));
   };
+  // row of 16-row block j of this wave within the tile
+  auto arow = [&](int j) { return (j * C::WM + wm) * 16; };
 
-  for (int kc = 0; kc < nk; ++kc) {
-    // this wave's copies of stage kc are done (later stages may stay in flight) ...
-    if (kc + C::STAGES - 2 < nk) {
-      wait_vmcnt<(C::STAGES - 2) * (C::A_DMA + C::B_DMA)>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    // ... and so are every other wave's; all reads of stage kc-1 are finished
-    barrier_raw();
-    if (kc + C::STAGES - 1 < nk) issue((kc + C::STAGES - 1) % C::STAGES, (kc + C::STAGES - 1) * BK);
-    if (mb_live > 0) {
-      const unsigned char* sa = smem + (kc % C::STAGES) * C::STAGE;
-      const unsigned char* sb = sa + C::A_BYTES;
-      read_frags(sa, sb, 0, 0);
+  int gs = 0;  // global step index of the consumer (ring slot = gs % S)
+  for (int ci = 0; ci < ntl; ++ci) {
+    const TileInfo ct = tile_of(ci);
+    const bool c_shared = ct.g >= E;
+    const bool c_priv = !c_shared && ct.g >= a.n_pub;
+    const int cI = c_shared ? a.Is : a.I;
+    const int cnk = (GATED ? H : cI) / BK;
+    const bool c_valid = !(c_priv && (a.w13_priv == nullptr || a.w2_priv == nullptr));
+    // this wave's blocks j with a valid row: (j * WM + wm) * 16 < rows
+    const int nblk = (ct.rows + 15) / 16;
+    const int mb_live = c_valid ? max(0, min(C::MB, (nblk - wm + C::WM - 1) / C::WM)) : 0;
+    for (int kc = 0; kc < cnk; ++kc, ++gs) {
+      // this wave's copies of step gs are done (the S-2 younger steps, when they were
+      // issued, may stay in flight) ...
+      if (issued - 1 - gs >= S - 2)
+        wait_vmcnt<(S - 2) * NDMA>();
+      else
+        wait_vmcnt<0>();
+      // ... and every other wave's; every read of step gs-1 is finished
+      barrier_raw();
+      produce((gs + S - 1) % S);
+      if (mb_live > 0) {
+        const int slot = gs % S;
+        if (FB == 2) read_frags(slot, 0, 0);
 #pragma unroll
-      for (int sub = 0; sub < SUB; ++sub) {
-        if (sub + 1 < SUB) read_frags(sa, sb, sub + 1, (sub + 1) & 1);
+        for (int sub = 0; sub < SUB; ++sub) {
+          const int cur = (FB == 2) ? (sub & 1) : 0;
+          if (FB == 2) {
+            if (sub + 1 < SUB) read_frags(slot, sub + 1, (sub + 1) & 1);
+          } else {
+            read_frags(slot, sub, 0);
+          }
+          // straight-line MFMAs (blocks past the valid rows compute rows that are never
+          // stored; a wave with no valid row skips the step entirely)
 #pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb) {
-          if (mb < mb_live) {
+          for (int mb = 0; mb < C::MB; ++mb)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[sub & 1][mb], fb[sub & 1][nb],
+              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[cur][mb], fb[cur][nb],
                                                                    acc[mb][nb], 0, 0, 0);
-          }
         }
       }
     }
-  }
-  __syncthreads();  // all MFMA reads of LDS done: reuse it for the output tile
 
-  // Output tile [BM][NCOLS] bf16 in LDS, then 16-byte stores of the valid part.
-  uint16_t* so = (uint16_t*)smem;
+    // Epilogue of tile ci through the ring slot just consumed (younger slots hold the
+    // next tile's operands in flight).
+    uint16_t* so = (uint16_t*)(smem + ((gs - 1) % S) * C::STAGE);
+    uint16_t* out;
+    size_t ld;
+    const int width = GATED ? cI : H;
+    if (GATED) {
+      out = (uint16_t*)(c_shared ? a.h_sh : a.h);
+      ld = (size_t)cI;
+    } else {
+      out = (uint16_t*)(c_shared ? a.y_shared : a.y_perm);
+      ld = (size_t)H;
+    }
+    constexpr int VPR = NCOLS / 8;  // 16-byte vectors per output row
+    if (c_valid) {
+      for (int pass = 0; pass < C::BM / ER; ++pass) {
+        barrier_raw();  // the slot's previous contents are no longer read
 #pragma unroll
-  for (int mb = 0; mb < C::MB; ++mb)
+        for (int mb = 0; mb < C::MB; ++mb) {
+          const int r0 = arow(mb);
+          if (r0 / ER == pass && mb < mb_live) {
 #pragma unroll
-    for (int nb = 0; nb < NBO; ++nb)
+            for (int nb = 0; nb < NBO; ++nb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wrow0 + mb * 16 + (lane >> 4) * 4 + i;
-        const int c = wn * WCOLS + nb * 16 + (lane & 15);
-        float v;
-        if (GATED)
-          v = silu(acc[mb][nb][i]) * acc[mb][nb + NBO][i];
-        else
-          v = acc[mb][nb][i];
-        so[r * NCOLS + c] = (uint16_t)f32_to_bf16_rne(v);
+              for (int i = 0; i < 4; ++i) {
+                const int r = r0 - pass * ER + (lane >> 4) * 4 + i;
+                const int c = wn * WCOLS + nb * 16 + (lane & 15);
+                const float v = GATED ? silu(acc[mb][nb][i]) * acc[mb][nb + NBO][i] : acc[mb][nb][i];
+                so[r * NCOLS + c] = (uint16_t)f32_to_bf16_rne(v);
+              }
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes landed
+        barrier_raw();
+        const int prow = min(ER, ct.rows - pass * ER);
+        for (int i = tid; i < prow * VPR; i += C::THREADS) {
+          const int r = i / VPR, v = i - r * VPR;
+          const int c = ct.n0 + v * 8;
+          if (c < width)
+            *(u32x4*)(out + (size_t)(ct.base + pass * ER + r) * ld + c) = *(const u32x4*)(so + r * NCOLS + v * 8);
+        }
       }
-  __syncthreads();
-  uint16_t* out;
-  size_t ld;
-  if (GATED) {
-    out = (uint16_t*)(shared ? a.h_sh : a.h);
-    ld = (size_t)I;
-  } else {
-    out = (uint16_t*)(shared ? a.y_shared : a.y_perm);
-    ld = (size_t)H;
+    } else if (!GATED) {
+      // private rows without private weights: not executed, not audited, y zeroed
+      if (tid == 0 && a.dev_status) atomicOr(a.dev_status, PMPE_DEV_PRIV_WEIGHTS_MISSING);
+      for (int i = tid; i < ct.rows * VPR; i += C::THREADS) {
+        const int r = i / VPR, v = i - r * VPR;
+        const int c = ct.n0 + v * 8;
+        if (c < width) *(u32x4*)(out + (size_t)(ct.base + r) * ld + c) = u32x4{0, 0, 0, 0};
+      }
+    }
+    // Execution audit: the first N tile of every executed private M tile counts its rows.
+    if (!GATED && c_priv && c_valid && ct.n0 == 0) {
+      for (int r = tid; r < ct.rows; r += C::THREADS) atomicAdd(&a.audit_rows[s_rt[ci % 3][r]], 1u);
+      if (ct.m0 == 0 && tid == 0 && a.audit_calls) atomicAdd(&a.audit_calls[ct.g - a.n_pub], 1u);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    barrier_raw();  // epilogue reads of the slot are done before it is refilled
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0, 0, 0, 0};
   }
-  constexpr int VPR = NCOLS / 8;  // 16-byte vectors per output row
-  for (int i = tid; i < t.rows * VPR; i += C::THREADS) {
-    const int r = i / VPR, v = i - r * VPR;
-    const int c = t.n0 + v * 8;
-    if (c < width) *(u32x4*)(out + (size_t)(t.base + r) * ld + c) = *(const u32x4*)(so + r * NCOLS + v * 8);
-  }
-
-  // Execution audit: the first N tile of every private M tile counts its rows once.
-  if (!GATED && priv && t.n0 == 0) {
-    for (int r = tid; r < t.rows; r += C::THREADS) atomicAdd(&a.audit_rows[a.row_token[t.base + r]], 1u);
-    if (t.m0 == 0 && tid == 0 && a.audit_calls) atomicAdd(&a.audit_calls[t.g - a.n_pub], 1u);
-  }
+  wait_vmcnt<0>();  // no copy may still be writing LDS when the block exits
 }
 
 // ---------------------------------------------------------------------------
@@ -518,23 +646,32 @@ hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) {
   if (a.act_bf16) {
     // Average rows per routed expert picks the tile shape.
     const bool large = (int64_t)a.T * a.k >= (int64_t)128 * E;
-    auto grid = [&](int BMv, int ncols, bool gemm1) {
+    int dev = 0, ncu = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      int v = 0;
+      if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ncu = v;
+    }
+    // Persistent grid: blocks resident at once (a multiple of the 8 XCDs), never more
+    // than the tiles there can be.
+    auto grid = [&](int BMv, int ncols, bool gemm1, int per_cu) {
       const int64_t w = gemm1 ? a.I : a.H;
       int64_t tiles = ((int64_t)a.T * a.k / BMv + E) * ((w + ncols - 1) / ncols);
       if (a.Is > 0) {
         const int64_t ws = gemm1 ? a.Is : a.H;
         tiles += ((a.T + BMv - 1) / BMv) * ((ws + ncols - 1) / ncols);
       }
-      return dim3((unsigned)tiles);
+      int64_t g = (int64_t)ncu * per_cu;
+      if (tiles < g) g = (tiles + 7) / 8 * 8;
+      return dim3((unsigned)g);
     };
     if (large) {
       using C = CfgLarge;
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true), dim3(C::THREADS), 0, s, a);
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false), dim3(C::THREADS), 0, s, a);
+      hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
     } else {
       using C = CfgSmall;
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true), dim3(C::THREADS), 0, s, a);
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false), dim3(C::THREADS), 0, s, a);
+      hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
     }
   } else {
     const int m_slots = (a.T * a.k + F32_BM - 1) / F32_BM + E;

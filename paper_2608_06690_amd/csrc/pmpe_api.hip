@@ -35,6 +35,10 @@ pmpe_status check_desc(const pmpe_layer_desc* d, int32_t T) {
   if (d->gate_mode != PMPE_GATE_RENORM_TOPK && d->gate_mode != PMPE_GATE_POOL_SOFTMAX)
     return PMPE_ERR_SHAPE;
   if ((int64_t)T * d->top_k > (int64_t)INT32_MAX / 2) return PMPE_ERR_SHAPE;
+  // the expert kernels address rows of x, x_perm and h with 32-bit element offsets
+  const int64_t wmax = d->hidden > d->inter ? d->hidden : d->inter;
+  if ((int64_t)T * d->top_k * wmax >= ((int64_t)1 << 32)) return PMPE_ERR_SHAPE;
+  if ((int64_t)T * d->n_shared * d->shared_inter >= ((int64_t)1 << 32)) return PMPE_ERR_SHAPE;
   return PMPE_OK;
 }
 
