@@ -30,6 +30,22 @@ METRIC = "MoE-layer tokens/s (Qwen3-30B-A3B shape) + % MFMA peak; decode % HBM B
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 CALLS = ["route", "dispatch", "expert_ffn", "combine", "audit"]
+COPY_BYTES = 1 << 30
+
+# HBM traffic of one pmpe_expert_ffn call on the Qwen-shaped layer, from rocprofv3
+# FETCH_SIZE and WRITE_SIZE (summed over its kernels, scaled by the counters' reading
+# for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
+# counters were taken on: any other source reports null.
+FFN_TRAFFIC_BYTES = {
+    "1edaa36e4917fe699b8a3499221145eed24812687172e2f33a35c17659d7fa36": 2_002_291_508,
+}
+
+
+def ffn_source_hash():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2608_06690_amd", "csrc", "ffn.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
 
 
 def parse():
@@ -43,6 +59,8 @@ def parse():
     p.add_argument("--cpu-reps", type=int, default=3, help="timed repetitions of the CPU oracle")
     p.add_argument("--decode-only", action="store_true",
                    help="time only the decode workload (for a separate kernel profile)")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="run only a plain 1 GiB device-to-device copy (counter calibration)")
     return p.parse_args()
 
 
@@ -192,6 +210,29 @@ def main():
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 5
+        # read-only stream: a sum over the same 1 GiB (writes one scalar)
+        e0.record()
+        for _ in range(5):
+            src.sum(dtype=torch.float32)
+        e1.record()
+        torch.cuda.synchronize()
+        ms_r = e0.elapsed_time(e1) / 5
+        print(json.dumps({"copy_bytes": COPY_BYTES, "copy_us": ms * 1e3,
+                          "read_plus_write_gbs": 2 * COPY_BYTES / (ms * 1e-3) / 1e9,
+                          "sum_us": ms_r * 1e3, "read_only_gbs": COPY_BYTES / (ms_r * 1e-3) / 1e9}),
+              flush=True)
+        return
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
         return
@@ -216,7 +257,8 @@ def main():
                    "policy": "4 allow + 4 deny requests", "router": "fp32", "experts": "bf16"},
         "roofline": {"kernel": "pmpe_expert_ffn (gemm1_bf16_kernel + gemm2_bf16_kernel)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": FFN_TRAFFIC_BYTES.get(ffn_source_hash()),
                      "flop_per_launch": ffn_flop, "avg_us": ffn_us,
                      "weight_bytes": w_bytes, "ai_flop_per_weight_byte": ai,
                      "attainable_tflops_at_hbm_peak": attainable,

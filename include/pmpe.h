@@ -95,6 +95,9 @@ typedef struct {
   int32_t w_dtype;      /* pmpe_dtype of expert weights; must equal act_dtype */
   int32_t gate_mode;    /* pmpe_gate_mode */
 } pmpe_layer_desc;
+/* The expert kernels use 32-bit byte offsets, so validation also requires fewer than
+ * 2^31 elements in: T*top_k*max(hidden, inter), T*hidden, T*n_shared*shared_inter,
+ * 2*inter*hidden (one expert's w13) and 2*n_shared*shared_inter*hidden. */
 
 /* Bytes of workspace that any call below may need for T tokens (the maximum over
  * the calls, so one buffer serves all of them). 0 if the descriptor is invalid. */

@@ -7,10 +7,10 @@
 //           depend on the order of the atomics). popcount(mask) is the chunk's
 //           histogram, and the rank of token t among the chunk's rows of expert e is
 //           popcount(mask_e & ((1 << t) - 1)).
-//  scan     one workgroup per expert: the expert's offset is the number of pairs of
-//           all lower experts; a scan over the chunks' counts gives each chunk's first
-//           row; expert_count and expert_offset are written.
-//  scatter  row = chunk base + rank; token_row[t*k+j] = row; row_token[row] = t.
+//  count    one workgroup per expert: expert_count and a scan over the chunks' counts
+//           (each chunk's first row within the expert).
+//  scatter  one workgroup per chunk: expert_offset is the exclusive scan of the counts;
+//           row = offset + chunk base + rank; token_row[t*k+j] = row; row_token[row] = t.
 //  gather   (optional) one wave per permuted row copies x[row_token[row]] to
 //           x_perm[row] in 16-byte vectors, so reads and writes are coalesced.
 // No order-dependent atomics: the permutation is deterministic. Expert ids outside
@@ -43,25 +43,14 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(DispatchArgs 
   for (int e = tid; e < a.E; e += DP_THREADS) a.mask[(size_t)c * a.E + e] = s_mask[e];
 }
 
-__global__ __launch_bounds__(DP_THREADS) void dispatch_scan_kernel(DispatchArgs a, int nchunks) {
-  __shared__ int s_red[DP_THREADS / 64];
+// One workgroup per expert e: count[e] and the scan of its column of chunk counts
+// (chunk_base relative to the expert's first row).
+__global__ __launch_bounds__(DP_THREADS) void dispatch_count_kernel(DispatchArgs a, int nchunks) {
   __shared__ int s_wsum[DP_THREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int e = blockIdx.x;
   const int E = a.E;
-  // offset[e]: all pairs of experts below e
-  int below = 0;
-  for (int i = tid; i < nchunks * e; i += DP_THREADS) {
-    const int c = i / e, ee = i - c * e;
-    below += popc64(a.mask[(size_t)c * E + ee]);
-  }
-  for (int off = 32; off > 0; off >>= 1) below += __shfl_xor(below, off, 64);
-  if (lane == 0) s_red[wave] = below;
-  __syncthreads();
-  int offset = 0;
-  for (int w = 0; w < DP_THREADS / 64; ++w) offset += s_red[w];
-  // this expert's column: exclusive scan of the chunk counts, DP_THREADS chunks at a time
-  int running = offset;
+  int running = 0;
   for (int c0 = 0; c0 < nchunks; c0 += DP_THREADS) {
     const int c = c0 + tid;
     const int v = (c < nchunks) ? popc64(a.mask[(size_t)c * E + e]) : 0;
@@ -76,16 +65,37 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scan_kernel(DispatchArgs 
     running += tot;
     __syncthreads();
   }
-  if (tid == 0) {
-    a.count[e] = running - offset;
-    a.offset[e] = offset;
-    if (e == E - 1) a.offset[E] = running;
-  }
+  if (tid == 0) a.count[e] = running;
 }
 
+// Scatter, one workgroup per chunk: the expert offsets are an exclusive scan of
+// count[] (recomputed in LDS by every block; block 0 writes expert_offset), then
+// row = offset[e] + chunk base + popcount of the chunk's earlier tokens of e.
 __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchArgs a) {
-  const int tid = threadIdx.x;
+  __shared__ int s_off[DP_MAX_E + 1];
+  __shared__ int s_wsum[DP_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = blockIdx.x;
+  const int E = a.E;
+  int running = 0;
+  for (int e0 = 0; e0 < E; e0 += DP_THREADS) {
+    const int e = e0 + tid;
+    const int v = (e < E) ? a.count[e] : 0;
+    const int incl = wave_incl_scan(v);
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int before = running;
+    for (int w = 0; w < wave; ++w) before += s_wsum[w];
+    if (e < E) s_off[e] = before + incl - v;
+    int tot = 0;
+    for (int w = 0; w < DP_THREADS / 64; ++w) tot += s_wsum[w];
+    running += tot;
+    __syncthreads();
+  }
+  if (tid == 0) s_off[E] = running;
+  __syncthreads();
+  if (c == 0)
+    for (int e = tid; e <= E; e += DP_THREADS) a.offset[e] = s_off[e];
   const int t0 = c * DP_TOK;
   const int np = min(DP_TOK, a.T - t0) * a.k;
   const size_t p0 = (size_t)t0 * a.k;
@@ -93,10 +103,10 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchAr
     const size_t p = p0 + i;
     const int e = a.topk_idx[p];
     int row = -1;
-    if (e >= 0 && e < a.E) {
+    if (e >= 0 && e < E) {
       const int tl = i / a.k;
-      const uint64_t below = (tl == 0) ? 0ull : (a.mask[(size_t)c * a.E + e] & ((1ull << tl) - 1ull));
-      row = a.chunk_base[(size_t)c * a.E + e] + popc64(below);
+      const uint64_t below = (tl == 0) ? 0ull : (a.mask[(size_t)c * E + e] & ((1ull << tl) - 1ull));
+      row = s_off[e] + a.chunk_base[(size_t)c * E + e] + popc64(below);
       a.row_token[row] = t0 + tl;
     }
     a.token_row[p] = row;
@@ -125,7 +135,7 @@ int dispatch_chunks(int T) { return (T + DP_TOK - 1) / DP_TOK; }
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
   const int nchunks = dispatch_chunks(a.T);
   hipLaunchKernelGGL(dispatch_hist_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
-  hipLaunchKernelGGL(dispatch_scan_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
+  hipLaunchKernelGGL(dispatch_count_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
   hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
   if (a.x_perm) {
     const int nrows = a.T * a.k;

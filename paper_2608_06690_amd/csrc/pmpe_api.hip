@@ -35,10 +35,15 @@ pmpe_status check_desc(const pmpe_layer_desc* d, int32_t T) {
   if (d->gate_mode != PMPE_GATE_RENORM_TOPK && d->gate_mode != PMPE_GATE_POOL_SOFTMAX)
     return PMPE_ERR_SHAPE;
   if ((int64_t)T * d->top_k > (int64_t)INT32_MAX / 2) return PMPE_ERR_SHAPE;
-  // the expert kernels address rows of x, x_perm and h with 32-bit element offsets
+  // the expert kernels address rows of x, x_perm, h and of one expert's weights with
+  // 32-bit byte offsets (bf16 elements, so fewer than 2^31 elements)
+  const int64_t lim = (int64_t)1 << 31;
   const int64_t wmax = d->hidden > d->inter ? d->hidden : d->inter;
-  if ((int64_t)T * d->top_k * wmax >= ((int64_t)1 << 32)) return PMPE_ERR_SHAPE;
-  if ((int64_t)T * d->n_shared * d->shared_inter >= ((int64_t)1 << 32)) return PMPE_ERR_SHAPE;
+  const int64_t ish = (int64_t)d->n_shared * d->shared_inter;
+  if ((int64_t)T * d->top_k * wmax >= lim) return PMPE_ERR_SHAPE;
+  if ((int64_t)T * ish >= lim) return PMPE_ERR_SHAPE;
+  if ((int64_t)T * d->hidden >= lim) return PMPE_ERR_SHAPE;
+  if (2 * (int64_t)d->inter * d->hidden >= lim || 2 * ish * d->hidden >= lim) return PMPE_ERR_SHAPE;
   return PMPE_OK;
 }
 

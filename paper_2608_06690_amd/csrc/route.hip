@@ -160,16 +160,24 @@ __device__ void topk_one_token(const TopkCtx& c, int t, int tau, const float* z)
 // their partial sums are added in fixed wave order, then the bias. Only tokens whose
 // policy selects this pool are fed (others are zero rows) and written.
 template <int TT>
-__global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs a) {
+__global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs a, int ntiles, int ngroups) {
   constexpr int NMB = TT / 16;
   __shared__ int s_tau[TT];
   __shared__ int s_any;
   __shared__ float s_part[RT_WAVES][TT][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t0 = blockIdx.x * TT;
+  // 1-D grid, (token tile, expert group) with the group fastest; XCD blockIdx % 8
+  // takes a contiguous range of that order, so a token tile is fetched into one L2.
+  const int total = ntiles * ngroups;
+  const int b = blockIdx.x, xcd = b & 7, j = b >> 3;
+  const int cnt_x = (total >> 3) + (xcd < (total & 7) ? 1 : 0);
+  if (j >= cnt_x) return;  // past this XCD's range
+  const int L = xcd * (total >> 3) + min(xcd, total & 7) + j;
+  const int tile = L / ngroups, grp = L - tile * ngroups;
+  const int t0 = tile * TT;
   const int gpub = (a.n_pub + 15) >> 4;
-  const int pass = blockIdx.y < gpub ? 0 : 1;
-  const int n0 = (pass ? blockIdx.y - gpub : blockIdx.y) * 16;
+  const int pass = grp < gpub ? 0 : 1;
+  const int n0 = (pass ? grp - gpub : grp) * 16;
   const int N = pass ? a.n_priv : a.n_pub;
   if (tid == 0) s_any = 0;
   __syncthreads();
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   }
   const int nsteps = H / (32 * RT_WAVES);  // K steps of this wave's quarter
   const int kbase = wave * nsteps;
-  const int rot = (blockIdx.x * 5 + blockIdx.y * 3) % nsteps;
+  const int rot = (tile * 5 + grp * 3) % nsteps;
   f32x4 acc[NMB];
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) acc[mb] = f32x4{0, 0, 0, 0};
@@ -302,10 +310,13 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   if (a.act_bf16) {
     const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
-    if (a.T > 2048)
-      hipLaunchKernelGGL(route_logits_bf16_kernel<32>, dim3((a.T + 31) / 32, groups), dim3(RT_THREADS), 0, s, a);
-    else
-      hipLaunchKernelGGL(route_logits_bf16_kernel<16>, dim3((a.T + 15) / 16, groups), dim3(RT_THREADS), 0, s, a);
+    if (a.T > 2048) {
+      const int nt = (a.T + 31) / 32;
+      hipLaunchKernelGGL(route_logits_bf16_kernel<32>, dim3((nt * groups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, groups);
+    } else {
+      const int nt = (a.T + 15) / 16;
+      hipLaunchKernelGGL(route_logits_bf16_kernel<16>, dim3((nt * groups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, groups);
+    }
   } else {
     hipLaunchKernelGGL(route_logits_f32_kernel, dim3(a.T), dim3(RT_THREADS), 0, s, a);
   }

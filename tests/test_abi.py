@@ -62,6 +62,8 @@ def test_valid_descriptor_and_workspace():
     (dict(hidden=100), -2), (dict(hidden=192), -2), (dict(inter=100), -2),
     (dict(n_pub=0), -2), (dict(n_pub=300), -2), (dict(n_priv=300), -2),
     (dict(n_shared=2, shared_inter=0), -2),
+    (dict(hidden=16384, inter=65536), -2),                       # one expert's w13 >= 2^31 elements
+    (dict(hidden=16384, inter=1024, n_shared=64, shared_inter=1024), -2),
 ])
 def test_invalid_descriptor_codes(kw, status):
     d = desc(**kw)
@@ -80,6 +82,9 @@ def test_dtype_and_gate_mode_codes():
     d.gate_mode = 5
     assert P.pmpe_check_desc(d, 16) == -2
     assert P.pmpe_check_desc(desc(), -1) == -2
+    # 32-bit byte offsets of the permuted rows: T*k*max(H, I) must stay below 2^31
+    assert P.pmpe_check_desc(desc(hidden=8192, top_k=8), 32768) == -2
+    assert P.pmpe_check_desc(desc(hidden=8192, top_k=8), 32767) == 0
 
 
 def fake(addr):
