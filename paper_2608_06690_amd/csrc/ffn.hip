@@ -55,8 +55,18 @@ __device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
 }
 // Same copy addressed as a wave-uniform 64-bit base (SGPRs) plus a per-lane 32-bit
 // byte offset; the LDS destination is a wave-uniform base plus the immediate IMM.
+// The base and the LDS address must be wave-uniform; they are passed through
+// readfirstlane so that they are held in SGPRs whatever the compiler can prove.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
 template <int IMM>
-__device__ __forceinline__ void dma16s(uint32_t byte_off, const void* base, uint32_t lds_base) {
+__device__ __forceinline__ void dma16s(uint32_t byte_off, const void* base_, uint32_t lds_base_) {
+  const void* base = uniform_ptr(base_);
+  const uint32_t lds_base = __builtin_amdgcn_readfirstlane(lds_base_);
   asm volatile(
       "s_add_u32 m0, %2, %3\n\t"
       "s_nop 0\n\t"
@@ -130,7 +140,8 @@ using CfgSmall = Cfg<PMPE_CFG_SMALL>;  // decode-shaped: 4 waves, 3 x 24 KiB sta
 constexpr int MAXG = 2 * PMPE_MAX_POOL + 1;  // routed experts + the shared group
 
 // DMA of 4 bytes per lane (int32 gather indices): lane l's word lands at lds_base + 4 * l.
-__device__ __forceinline__ void dma4(const void* src, uint32_t lds_base) {
+__device__ __forceinline__ void dma4(const void* src, uint32_t lds_base_) {
+  const uint32_t lds_base = __builtin_amdgcn_readfirstlane(lds_base_);
   asm volatile(
       "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
@@ -310,7 +321,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     return K / BK;
   };
   auto issue = [&](int slot, int k0) {
-    const uint32_t sa = lds0 + slot * C::STAGE;
+    // slot is wave-uniform; say so, so that the LDS base stays in an SGPR
+    const uint32_t sa = __builtin_amdgcn_readfirstlane(lds0 + slot * C::STAGE);
     const uint32_t sb = sa + C::A_BYTES;
     const uint16_t* ba = baseA + k0;  // scalar bases advance by the K step
     const uint16_t* bb = baseB + k0;
@@ -346,12 +358,6 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
 #pragma unroll
   for (int s = 0; s < S - 1; ++s) produce(s);
 
-  f32x4 acc[C::MB][NB];
-#pragma unroll
-  for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0, 0, 0, 0};
-
   // B operand row (within the tile) of block nb of this wave, minus the wave's offset
   auto bconst = [&](int nb) {
     if (GATED) return (nb < NBO) ? nb * 16 : C::BN / 2 + (nb - NBO) * 16;
@@ -366,29 +372,57 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   uint32_t lane_off[SUB];
 #pragma unroll
   for (int sub = 0; sub < SUB; ++sub) lane_off[sub] = (uint32_t)swz<BK>(lane & 15, sub * 4 + (lane >> 4));
-  auto read_frags = [&](int slot, int sub, int buf) {
+  // Fragments of K sub-step `sub`: all NB operand blocks of B, and the first MBL
+  // 16-row blocks of A (the blocks past MBL hold no valid row of the tile).
+  auto read_frags = [&](auto mbl, int slot, int sub, int buf) {
+    constexpr int MBL = decltype(mbl)::value;
     const uint32_t pa = lane_off[sub] + slot * C::STAGE + wm * 16 * C::RB;
     const uint32_t pb = lane_off[sub] + slot * C::STAGE + C::A_BYTES + wn * WCOLS * C::RB;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) fb[buf][nb] = as_bf16x8(*(const u32x4*)(smem + pb + bconst(nb) * C::RB));
 #pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
+    for (int mb = 0; mb < MBL; ++mb)
       fa[buf][mb] = as_bf16x8(*(const u32x4*)(smem + pa + mb * C::WM * 16 * C::RB));
+  };
+  // One K step on the first MBL row blocks of this wave.
+  auto kstep = [&](auto mbl, int slot, f32x4 (&acc)[decltype(mbl)::value][NB]) {
+    constexpr int MBL = decltype(mbl)::value;
+    if (FB == 2) read_frags(mbl, slot, 0, 0);
+#pragma unroll
+    for (int sub = 0; sub < SUB; ++sub) {
+      const int cur = (FB == 2) ? (sub & 1) : 0;
+      if (FB == 2) {
+        if (sub + 1 < SUB) read_frags(mbl, slot, sub + 1, (sub + 1) & 1);
+      } else {
+        read_frags(mbl, slot, sub, 0);
+      }
+#pragma unroll
+      for (int mb = 0; mb < MBL; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[cur][mb], fb[cur][nb],
+                                                               acc[mb][nb], 0, 0, 0);
+      // single-buffered fragments: keep the next sub-step's reads below these MFMAs
+      if (FB == 1) __builtin_amdgcn_sched_barrier(0);
+    }
   };
   // row of 16-row block j of this wave within the tile
   auto arow = [&](int j) { return (j * C::WM + wm) * 16; };
 
   int gs = 0;  // global step index of the consumer (ring slot = gs % S)
-  for (int ci = 0; ci < ntl; ++ci) {
-    const TileInfo ct = tile_of(ci);
-    const bool c_shared = ct.g >= E;
-    const bool c_priv = !c_shared && ct.g >= a.n_pub;
-    const int cI = c_shared ? a.Is : a.I;
-    const int cnk = (GATED ? H : cI) / BK;
-    const bool c_valid = !(c_priv && (a.w13_priv == nullptr || a.w2_priv == nullptr));
-    // this wave's blocks j with a valid row: (j * WM + wm) * 16 < rows
-    const int nblk = (ct.rows + 15) / 16;
-    const int mb_live = c_valid ? max(0, min(C::MB, (nblk - wm + C::WM - 1) / C::WM)) : 0;
+  constexpr int VPR = NCOLS / 8;  // 16-byte vectors per output row
+  // K loop and output of one tile for a wave whose valid row blocks all lie in its
+  // first MBL blocks. The accumulators live only here, so the variants for fully and
+  // partly filled tiles share no loop-carried registers. Every variant runs the same
+  // sequence of barriers (one per K step, two per epilogue pass).
+  auto tile_body = [&](auto mbl, const TileInfo& ct, int cnk, int mb_live, bool c_valid,
+                       uint16_t* out, size_t ld, int width) {
+    constexpr int MBL = decltype(mbl)::value;
+    f32x4 acc[MBL][NB];
+#pragma unroll
+    for (int mb = 0; mb < MBL; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0, 0, 0, 0};
     for (int kc = 0; kc < cnk; ++kc, ++gs) {
       // this wave's copies of step gs are done (the S-2 younger steps, when they were
       // issued, may stay in flight) ...
@@ -399,32 +433,53 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
       // ... and every other wave's; every read of step gs-1 is finished
       barrier_raw();
       produce((gs + S - 1) % S);
-      if (mb_live > 0) {
-        const int slot = gs % S;
-        if (FB == 2) read_frags(slot, 0, 0);
+      // straight-line MFMAs (rows past the valid count inside a live block are
+      // computed but never stored; a wave with no valid row skips the step)
+      if (mb_live > 0) kstep(mbl, gs % S, acc);
+    }
+    if (!c_valid) return;
+    // Epilogue through the ring slot just consumed (younger slots hold the next
+    // tile's operands in flight).
+    uint16_t* so = (uint16_t*)(smem + ((gs - 1) % S) * C::STAGE);
+    for (int pass = 0; pass < C::BM / ER; ++pass) {
+      barrier_raw();  // the slot's previous contents are no longer read
 #pragma unroll
-        for (int sub = 0; sub < SUB; ++sub) {
-          const int cur = (FB == 2) ? (sub & 1) : 0;
-          if (FB == 2) {
-            if (sub + 1 < SUB) read_frags(slot, sub + 1, (sub + 1) & 1);
-          } else {
-            read_frags(slot, sub, 0);
-          }
-          // straight-line MFMAs (blocks past the valid rows compute rows that are never
-          // stored; a wave with no valid row skips the step entirely)
+      for (int mb = 0; mb < MBL; ++mb) {
+        const int r0 = arow(mb);
+        if (r0 / ER == pass && mb < mb_live) {
 #pragma unroll
-          for (int mb = 0; mb < C::MB; ++mb)
+          for (int nb = 0; nb < NBO; ++nb)
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[cur][mb], fb[cur][nb],
-                                                                   acc[mb][nb], 0, 0, 0);
+            for (int i = 0; i < 4; ++i) {
+              const int r = r0 - pass * ER + (lane >> 4) * 4 + i;
+              const int c = wn * WCOLS + nb * 16 + (lane & 15);
+              const float v = GATED ? silu(acc[mb][nb][i]) * acc[mb][nb + NBO][i] : acc[mb][nb][i];
+              so[r * NCOLS + c] = (uint16_t)f32_to_bf16_rne(v);
+            }
         }
       }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes landed
+      barrier_raw();
+      const int prow = min(ER, ct.rows - pass * ER);
+      for (int i = tid; i < prow * VPR; i += C::THREADS) {
+        const int r = i / VPR, v = i - r * VPR;
+        const int c = ct.n0 + v * 8;
+        if (c < width)
+          *(u32x4*)(out + (size_t)(ct.base + pass * ER + r) * ld + c) = *(const u32x4*)(so + r * NCOLS + v * 8);
+      }
     }
+  };
 
-    // Epilogue of tile ci through the ring slot just consumed (younger slots hold the
-    // next tile's operands in flight).
-    uint16_t* so = (uint16_t*)(smem + ((gs - 1) % S) * C::STAGE);
+  for (int ci = 0; ci < ntl; ++ci) {
+    const TileInfo ct = tile_of(ci);
+    const bool c_shared = ct.g >= E;
+    const bool c_priv = !c_shared && ct.g >= a.n_pub;
+    const int cI = c_shared ? a.Is : a.I;
+    const int cnk = (GATED ? H : cI) / BK;
+    const bool c_valid = !(c_priv && (a.w13_priv == nullptr || a.w2_priv == nullptr));
+    // this wave's blocks j with a valid row: (j * WM + wm) * 16 < rows
+    const int nblk = (ct.rows + 15) / 16;
+    const int mb_live = c_valid ? max(0, min(C::MB, (nblk - wm + C::WM - 1) / C::WM)) : 0;
     uint16_t* out;
     size_t ld;
     const int width = GATED ? cI : H;
@@ -435,36 +490,14 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
       out = (uint16_t*)(c_shared ? a.y_shared : a.y_perm);
       ld = (size_t)H;
     }
-    constexpr int VPR = NCOLS / 8;  // 16-byte vectors per output row
-    if (c_valid) {
-      for (int pass = 0; pass < C::BM / ER; ++pass) {
-        barrier_raw();  // the slot's previous contents are no longer read
-#pragma unroll
-        for (int mb = 0; mb < C::MB; ++mb) {
-          const int r0 = arow(mb);
-          if (r0 / ER == pass && mb < mb_live) {
-#pragma unroll
-            for (int nb = 0; nb < NBO; ++nb)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                const int r = r0 - pass * ER + (lane >> 4) * 4 + i;
-                const int c = wn * WCOLS + nb * 16 + (lane & 15);
-                const float v = GATED ? silu(acc[mb][nb][i]) * acc[mb][nb + NBO][i] : acc[mb][nb][i];
-                so[r * NCOLS + c] = (uint16_t)f32_to_bf16_rne(v);
-              }
-          }
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes landed
-        barrier_raw();
-        const int prow = min(ER, ct.rows - pass * ER);
-        for (int i = tid; i < prow * VPR; i += C::THREADS) {
-          const int r = i / VPR, v = i - r * VPR;
-          const int c = ct.n0 + v * 8;
-          if (c < width)
-            *(u32x4*)(out + (size_t)(ct.base + pass * ER + r) * ld + c) = *(const u32x4*)(so + r * NCOLS + v * 8);
-        }
-      }
-    } else if (!GATED) {
+    // A partly filled tile (e.g. an expert with fewer rows than BM) runs the variant
+    // that reads and multiplies only the first half of the wave's row blocks.
+    if (C::MB >= 2 && mb_live <= C::MB / 2)
+      tile_body(std::integral_constant<int, (C::MB >= 2 ? C::MB / 2 : C::MB)>{}, ct, cnk, mb_live,
+                c_valid, out, ld, width);
+    else
+      tile_body(std::integral_constant<int, C::MB>{}, ct, cnk, mb_live, c_valid, out, ld, width);
+    if (!c_valid && !GATED) {
       // private rows without private weights: not executed, not audited, y zeroed
       if (tid == 0 && a.dev_status) atomicOr(a.dev_status, PMPE_DEV_PRIV_WEIGHTS_MISSING);
       for (int i = tid; i < ct.rows * VPR; i += C::THREADS) {
@@ -480,10 +513,6 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
     barrier_raw();  // epilogue reads of the slot are done before it is refilled
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0, 0, 0, 0};
   }
   wait_vmcnt<0>();  // no copy may still be writing LDS when the block exits
 }

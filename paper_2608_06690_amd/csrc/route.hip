@@ -158,12 +158,12 @@ __device__ void topk_one_token(const TopkCtx& c, int t, int tau, const float* z)
 // one pool; the four waves split H in quarters (each wave starts its quarter at a
 // block-dependent step so that concurrent blocks read different router columns) and
 // their partial sums are added in fixed wave order, then the bias. Only tokens whose
-// policy selects this pool are fed (others are zero rows) and written.
+// policy selects this pool are fed and written.
 template <int TT>
 __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs a, int ntiles, int ngroups) {
   constexpr int NMB = TT / 16;
   __shared__ int s_tau[TT];
-  __shared__ int s_any;
+  __shared__ int s_first;
   __shared__ float s_part[RT_WAVES][TT][16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // 1-D grid, (token tile, expert group) with the group fastest; XCD blockIdx % 8
@@ -179,29 +179,33 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   const int pass = grp < gpub ? 0 : 1;
   const int n0 = (pass ? grp - gpub : grp) * 16;
   const int N = pass ? a.n_priv : a.n_pub;
-  if (tid == 0) s_any = 0;
+  if (tid == 0) s_first = TT;
   __syncthreads();
+  int mine = 0;
   if (tid < TT) {
     const int tau = (t0 + tid < a.T) ? token_tau(a, t0 + tid) : -1;
     s_tau[tid] = tau;
-    if (tau == pass) s_any = 1;
+    mine = (tau == pass) ? 1 : 0;
+    if (mine) atomicMin(&s_first, tid);
   }
-  __syncthreads();
-  if (!s_any) return;  // no token of this pool's policy in the tile: rows never read
+  // no token of this pool's policy in the tile: its router rows are never read
+  if (!__syncthreads_or(mine)) return;
   const float* wr = pass ? a.wr_priv : a.wr_pub;
   const int H = a.H;
   const uint16_t* x = (const uint16_t*)a.x;
+  // Operand rows of this lane. A lane whose expert is past the pool, or whose token
+  // has the other policy, reads a row that belongs to this pass (expert n0, the
+  // tile's first token of this policy) and its results are discarded: a token's x
+  // is only ever loaded for the pool its policy permits.
   const int n = n0 + (lane & 15);
-  const bool nv = n < N;
   const int koff = (lane >> 4) * 8;
-  const float* wrow = wr + (size_t)(nv ? n : n0) * H + koff;
+  const float* wrow = wr + (size_t)(n < N ? n : n0) * H + koff;
+  const int first = s_first;
   const uint16_t* xrow[NMB];
-  bool av[NMB];
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) {
     const int tt = mb * 16 + (lane & 15);
-    av[mb] = s_tau[tt] == pass;
-    xrow[mb] = x + (size_t)(av[mb] ? t0 + tt : t0) * H + koff;
+    xrow[mb] = x + (size_t)(t0 + (s_tau[tt] == pass ? tt : first)) * H + koff;
   }
   const int nsteps = H / (32 * RT_WAVES);  // K steps of this wave's quarter
   const int kbase = wave * nsteps;
@@ -209,48 +213,55 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   f32x4 acc[NMB];
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) acc[mb] = f32x4{0, 0, 0, 0};
-  constexpr int D = 4;  // K steps per batch of loads in flight
-  for (int s0 = 0; s0 < nsteps; s0 += D) {
-    float4 w[D][2];
-    u32x4 xa[D][NMB];
+  // A ring of D K steps of loads in flight. Loads are unconditional (a step past the
+  // end reloads the last one and is not used), so the loop is straight-line and the
+  // compiler's wait counts keep the ring full; each refill stays right after the
+  // step that freed its slot.
+  constexpr int D = 4;
+  float4 w[D][2];
+  u32x4 xa[D][NMB];
+  auto load = [&](int d, int st) {
+    st = min(st, nsteps - 1);
+    const int kk = (kbase + (st + rot) % nsteps) * 32;
+    w[d][0] = *(const float4*)(wrow + kk);
+    w[d][1] = *(const float4*)(wrow + kk + 4);
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      int st = s0 + d;
-      const bool sv = st < nsteps;
-      st = (st + rot) % nsteps;
-      const int kk = (kbase + st) * 32;
-      w[d][0] = make_float4(0, 0, 0, 0);
-      w[d][1] = w[d][0];
-      if (sv && nv) {
-        w[d][0] = *(const float4*)(wrow + kk);
-        w[d][1] = *(const float4*)(wrow + kk + 4);
-      }
+    for (int mb = 0; mb < NMB; ++mb) xa[d][mb] = *(const u32x4*)(xrow[mb] + kk);
+  };
+  auto step = [&](int d) {
+    const float wv[8] = {w[d][0].x, w[d][0].y, w[d][0].z, w[d][0].w,
+                         w[d][1].x, w[d][1].y, w[d][1].z, w[d][1].w};
+    uint32_t ph[8], pm[8], pl[8];
 #pragma unroll
-      for (int mb = 0; mb < NMB; ++mb)
-        xa[d][mb] = (sv && av[mb]) ? *(const u32x4*)(xrow[mb] + kk) : u32x4{0, 0, 0, 0};
+    for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
+    const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
+                                      ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
+    const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
+                                      pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
+    const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
+                                      pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+      const bf16x8 av8 = as_bf16x8(xa[d][mb]);
+      acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[mb], 0, 0, 0);
+      acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[mb], 0, 0, 0);
+      acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[mb], 0, 0, 0);
     }
+  };
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(d, d);
+  const int nfull = nsteps - nsteps % D;
+  for (int s0 = 0; s0 < nfull; s0 += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
-      const float wv[8] = {w[d][0].x, w[d][0].y, w[d][0].z, w[d][0].w,
-                           w[d][1].x, w[d][1].y, w[d][1].z, w[d][1].w};
-      uint32_t ph[8], pm[8], pl[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
-      const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
-                                        ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
-      const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
-                                        pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
-      const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
-                                        pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
-#pragma unroll
-      for (int mb = 0; mb < NMB; ++mb) {
-        const bf16x8 av8 = as_bf16x8(xa[d][mb]);
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[mb], 0, 0, 0);
-      }
+      step(d);
+      load(d, s0 + d + D);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (nfull + d < nsteps) step(d);
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
