@@ -37,7 +37,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "1edaa36e4917fe699b8a3499221145eed24812687172e2f33a35c17659d7fa36": 2_002_291_508,
+    "229a0e40470570fdb51fe035597bb685fd7a989185ac46d3ef10dd64cf04b8ba": 1_990_760_667,
 }
 
 
@@ -59,12 +59,18 @@ def parse():
     p.add_argument("--cpu-reps", type=int, default=3, help="timed repetitions of the CPU oracle")
     p.add_argument("--decode-only", action="store_true",
                    help="time only the decode workload (for a separate kernel profile)")
+    p.add_argument("--all-deny", action="store_true",
+                   help="run only the Qwen-shaped layer with every request denied (the expert FFN "
+                        "must then read public expert weights only)")
+    p.add_argument("--no-private-weights", action="store_true",
+                   help="with --all-deny: pass NULL for every private tensor (router rows and "
+                        "expert weights); the counters must read the same bytes as with them present")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="run only a plain 1 GiB device-to-device copy (counter calibration)")
     return p.parse_args()
 
 
-def setup(cfg_name, device):
+def setup(cfg_name, device, all_deny=False, drop_private=False):
     import torch
     import workloads as W
     import paper_2608_06690_amd as P
@@ -74,10 +80,17 @@ def setup(cfg_name, device):
     gm = P.PMPE_GATE_POOL_SOFTMAX if cfg.gate_mode == "pool_softmax" else P.PMPE_GATE_RENORM_TOPK
     desc = P.make_desc(cfg.hidden, cfg.inter, cfg.n_pub, cfg.n_priv, cfg.top_k, cfg.n_shared,
                        cfg.shared_inter, cfg.dtype == "bf16", gm)
-    layer = P.PolicyMaskedMoE(desc, Lw.wr_pub, Lw.wr_priv, Lw.bias, Lw.w13_pub, Lw.w2_pub,
-                              Lw.w13_priv, Lw.w2_priv, Lw.w13_sh, Lw.w2_sh)
+    if drop_private:
+        layer = P.PolicyMaskedMoE(desc, Lw.wr_pub, None, Lw.bias, Lw.w13_pub, Lw.w2_pub,
+                                  None, None, Lw.w13_sh, Lw.w2_sh)
+    else:
+        layer = P.PolicyMaskedMoE(desc, Lw.wr_pub, Lw.wr_priv, Lw.bias, Lw.w13_pub, Lw.w2_pub,
+                                  Lw.w13_priv, Lw.w2_priv, Lw.w13_sh, Lw.w2_sh)
     x = W.make_x(cfg, device)
     req = W.make_requests(cfg, 0)
+    if all_deny:
+        req = W.Requests(list(req.lengths), [dict(W.DENY_META) for _ in req.lengths],
+                         ["deny"] * len(req.lengths))
     words = P.token_policy_words(req.metas, req.lengths, device)
     req_off = P.request_offsets(req.lengths, device)
     audit = layer.audit_buffers(cfg.tokens, len(req.lengths))
@@ -133,13 +146,26 @@ def time_layer(layer, x, words, req_off, audit, bufs, steps, warmup, flush=None)
             per[c].append(ev[i].elapsed_time(ev[i + 1]) * 1e3)  # us
     med = {c: sorted(v)[len(v) // 2] for c, v in per.items()}
     mean = {c: sum(v) / len(v) for c, v in per.items()}
-    return wall / steps * 1e3, med, mean
+    p10 = {c: sorted(v)[len(v) // 10] for c, v in per.items()}
+    p90 = {c: sorted(v)[min(len(v) - 1, (9 * len(v)) // 10)] for c, v in per.items()}
+    return wall / steps * 1e3, med, mean, p10, p90
 
 
-def cpu_baseline(cfg, req, n_sample, reps):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, req, n_sample, reps, min_seconds=10.0):
     """The CPU oracle on a bounded sample: n_sample tokens (half from allow requests,
-    half from deny requests), routed and run through their experts; the median of
-    `reps` timed repetitions."""
+    half from deny requests), routed and run through their experts; the median of at
+    least `reps` timed repetitions, repeated until about `min_seconds` of CPU work."""
     import numpy as np
     import torch
     from oracle import pmpe_oracle as O
@@ -162,7 +188,7 @@ def cpu_baseline(cfg, req, n_sample, reps):
         w2[e] = b.double().numpy()
     words = words_all[toks]
     times = []
-    for _ in range(reps):
+    while len(times) < reps or (sum(times) < min_seconds and len(times) < 50):
         t0 = time.perf_counter()
         res = O.layer_forward(x, wr_pub, wr_priv, bias, w13[:cfg.n_pub], w2[:cfg.n_pub],
                               w13[cfg.n_pub:], w2[cfg.n_pub:], words, cfg.top_k, cfg.gate_mode)
@@ -173,7 +199,8 @@ def cpu_baseline(cfg, req, n_sample, reps):
             "kind": "oracle",
             "sample": f"{len(toks)} of the {cfg.tokens} tokens ({n_sample // 2} allow, "
                       f"{n_sample - n_sample // 2} deny), whole layer in fp64 numpy; median of "
-                      f"{reps} runs, {dt:.1f} s each"}
+                      f"{len(times)} runs, {dt:.2f} s each, {sum(times):.1f} s in all; "
+                      f"CPU {cpu_model()}"}
 
 
 def decode_bench(args, dev):
@@ -183,7 +210,7 @@ def decode_bench(args, dev):
     import torch
     cfgd, layerd, xd, wd, rod, ad, bd, _ = setup("decode", dev)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    msd, medd, meand = time_layer(layerd, xd, wd, rod, ad, bd, args.steps, args.warmup, flush)
+    msd, medd, meand, p10d, p90d = time_layer(layerd, xd, wd, rod, ad, bd, args.steps, args.warmup, flush)
     counts = bd.expert_count.cpu()
     touched = int((counts > 0).sum())
     wb = touched * 3 * cfgd.hidden * cfgd.inter * 2
@@ -193,6 +220,7 @@ def decode_bench(args, dev):
            "experts_touched": touched, "weight_bytes": wb,
            "ffn_us_mean": meand["expert_ffn"], "ffn_hbm_gbs": gbs,
            "ffn_hbm_frac": gbs / PEAK_HBM_GBS, "calls_us_mean": meand,
+           "calls_us_median": medd, "calls_us_p10": p10d, "calls_us_p90": p90d,
            "note": "L2/MALL flushed by a 512 MiB write before each event-timed step"}
     del layerd, xd, bd, flush
     torch.cuda.empty_cache()
@@ -221,23 +249,28 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / 5
-        # read-only stream: a sum over the same 1 GiB (writes one scalar)
-        e0.record()
-        for _ in range(5):
-            src.sum(dtype=torch.float32)
-        e1.record()
-        torch.cuda.synchronize()
-        ms_r = e0.elapsed_time(e1) / 5
         print(json.dumps({"copy_bytes": COPY_BYTES, "copy_us": ms * 1e3,
-                          "read_plus_write_gbs": 2 * COPY_BYTES / (ms * 1e-3) / 1e9,
-                          "sum_us": ms_r * 1e3, "read_only_gbs": COPY_BYTES / (ms_r * 1e-3) / 1e9}),
-              flush=True)
+                          "read_plus_write_gbs": 2 * COPY_BYTES / (ms * 1e-3) / 1e9}), flush=True)
         return
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
         return
+    if args.all_deny:
+        cfg, layer, x, words, req_off, audit, bufs, req = setup("qwen", dev, all_deny=True,
+                                                                drop_private=args.no_private_weights)
+        ms, med, mean, p10, p90 = time_layer(layer, x, words, req_off, audit, bufs, args.steps, args.warmup)
+        counts = bufs.expert_count.cpu()
+        touched = int((counts > 0).sum())
+        print(json.dumps({"workload": "qwen3-30b-a3b-shaped layer, 8 requests x 512 tokens, all denied",
+                          "private_tensors": "NULL" if args.no_private_weights else "present",
+                          "ms_per_step": ms, "private_rows_routed": int(counts[cfg.n_pub:].sum()),
+                          "private_rows_executed": int(audit.total.item()),
+                          "public_experts_touched": touched,
+                          "public_weight_bytes": touched * 3 * cfg.hidden * cfg.inter * 2,
+                          "calls_us_mean": mean}), flush=True)
+        return
     cfg, layer, x, words, req_off, audit, bufs, req = setup("qwen", dev)
-    ms, med, mean = time_layer(layer, x, words, req_off, audit, bufs, args.steps, args.warmup)
+    ms, med, mean, p10, p90 = time_layer(layer, x, words, req_off, audit, bufs, args.steps, args.warmup)
     T = cfg.tokens
     pairs = T * cfg.top_k
     ffn_flop = pairs * 2 * 3 * cfg.hidden * cfg.inter
@@ -255,7 +288,7 @@ def main():
                    "requests": cfg.requests, "hidden": cfg.hidden, "inter": cfg.inter,
                    "n_pub": cfg.n_pub, "n_priv": cfg.n_priv, "top_k": cfg.top_k,
                    "policy": "4 allow + 4 deny requests", "router": "fp32", "experts": "bf16"},
-        "roofline": {"kernel": "pmpe_expert_ffn (gemm1_bf16_kernel + gemm2_bf16_kernel)",
+        "roofline": {"kernel": "pmpe_expert_ffn (gemm_bf16_kernel GEMM1 + GEMM2)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": FFN_TRAFFIC_BYTES.get(ffn_source_hash()),
@@ -263,7 +296,7 @@ def main():
                      "weight_bytes": w_bytes, "ai_flop_per_weight_byte": ai,
                      "attainable_tflops_at_hbm_peak": attainable,
                      "attainable_frac": achieved / attainable},
-        "calls_us_mean": mean, "calls_us_median": med,
+        "calls_us_mean": mean, "calls_us_median": med, "calls_us_p10": p10, "calls_us_p90": p90,
     }
     del layer, x, bufs
     torch.cuda.empty_cache()

@@ -112,10 +112,13 @@ __device__ __forceinline__ int swz(int r, int c) {
     return r * 64 + ((c ^ ((r >> 1) & 3)) << 4);
 }
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_, int FRAG_BUFS_ = 1>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_, int FRAG_BUFS_ = 1, bool HALF_ = true>
 struct Cfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, BK = BK_;
   static constexpr int FRAG_BUFS = FRAG_BUFS_;  // 2: read the next K step's fragments early
+  // a shorter K-loop variant for tiles whose valid rows fill at most half of each wave's
+  // row blocks (needs the registers of a second accumulator set)
+  static constexpr bool HALF = HALF_;
   static constexpr int RB = 2 * BK, CH = BK / 8, RPD = 1024 / RB;  // rows per DMA instruction
   static constexpr int WAVES = WM * WN, THREADS = 64 * WAVES;
   static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB, STAGE = A_BYTES + B_BYTES;
@@ -150,6 +153,14 @@ __device__ __forceinline__ void dma4(const void* src, uint32_t lds_base_) {
       : "memory", "m0");
 }
 
+// Rows of the output tile staged per epilogue pass: the largest multiple of 16 that
+// divides BM and whose bf16 rows fit in one ring stage.
+constexpr int epilogue_rows(int fit, int bm) {
+  for (int d = (fit < bm ? fit : bm) / 16 * 16; d >= 16; d -= 16)
+    if (bm % d == 0) return d;
+  return 16;
+}
+
 struct TileInfo {
   int g;     // group: expert id, or E for the shared group
   int m0;    // first row of the tile within the group
@@ -180,7 +191,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   constexpr int NBO = WCOLS / 16;                    // output 16-col blocks per wave
   constexpr int NB = GATED ? 2 * NBO : NBO;          // B operand blocks per wave
   constexpr int BK = C::BK, S = C::STAGES, NDMA = C::A_DMA + C::B_DMA;
-  constexpr int ER = (C::STAGE / (NCOLS * 2)) < C::BM ? (C::STAGE / (NCOLS * 2)) : C::BM;  // epilogue rows per pass
+  constexpr int ER = epilogue_rows(C::STAGE / (NCOLS * 2), C::BM);  // epilogue rows per pass
   static_assert(ER % 16 == 0 && C::BM % ER == 0, "an epilogue pass must hold whole 16-row blocks");
   static_assert(C::BM % 64 == 0 || C::BM <= 64, "row_token slice copy");
 
@@ -492,7 +503,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     }
     // A partly filled tile (e.g. an expert with fewer rows than BM) runs the variant
     // that reads and multiplies only the first half of the wave's row blocks.
-    if (C::MB >= 2 && mb_live <= C::MB / 2)
+    if (C::HALF && C::MB >= 2 && mb_live <= C::MB / 2)
       tile_body(std::integral_constant<int, (C::MB >= 2 ? C::MB / 2 : C::MB)>{}, ct, cnk, mb_live,
                 c_valid, out, ld, width);
     else
