@@ -37,7 +37,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "229a0e40470570fdb51fe035597bb685fd7a989185ac46d3ef10dd64cf04b8ba": 1_990_760_667,
+    "cd034d5d698ab77b4c7d8e726c6d26db55e08810929df7df5a74c83d480792e6": 1_989_802_093,
 }
 
 
