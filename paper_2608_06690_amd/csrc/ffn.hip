@@ -208,7 +208,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   constexpr int BK = C::BK, S = C::STAGES, NDMA = C::A_DMA + C::B_DMA;
   constexpr int ER = epilogue_rows(C::STAGE / (NCOLS * 2), C::BM);  // epilogue rows per pass
   static_assert(ER % 16 == 0 && C::BM % ER == 0, "an epilogue pass must hold whole 16-row blocks");
-  static_assert(C::BM % 64 == 0 || C::BM <= 64, "row_token slice copy");
+  static_assert(C::BM % 64 == 0, "row_token slices are copied 64 entries at a time");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int uwave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, scalar
@@ -241,10 +241,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   // This block's tiles: L_i = start_x + q + i * nbx, i < ntl.
   const int total = s_cum[ngroups];
   const int b = blockIdx.x, x = b & 7, q = b >> 3;
-  const int nbx = ((int)gridDim.x - x + 7) >> 3;
   const int cnt_x = (total >> 3) + (x < (total & 7) ? 1 : 0);
+  const int nbx = ((int)gridDim.x - x + 7) >> 3;
   const int start_x = x * (total >> 3) + min(x, total & 7);
-  const int ntl = (cnt_x > q) ? (cnt_x - q + nbx - 1) / nbx : 0;
+  const int ntl = (cnt_x > q && q < nbx) ? (cnt_x - q + nbx - 1) / nbx : 0;
   if (ntl == 0) return;
 
   auto tile_of = [&](int i) {

@@ -213,11 +213,11 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   f32x4 acc[NMB];
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) acc[mb] = f32x4{0, 0, 0, 0};
-  // A ring of D K steps of loads in flight. Loads are unconditional (a step past the
-  // end reloads the last one and is not used), so the loop is straight-line and the
-  // compiler's wait counts keep the ring full; each refill stays right after the
-  // step that freed its slot.
-  constexpr int D = 4;
+  // A ring of D K steps of loads (D-1 in flight while one is multiplied). Loads are
+  // unconditional (a step past the end reloads the last one and is not used), so the
+  // loop is straight-line and the compiler's wait counts keep the ring full; each
+  // refill stays right after the step that freed its slot.
+  constexpr int D = 2;
   float4 w[D][2];
   u32x4 xa[D][NMB];
   auto load = [&](int d, int st) {
