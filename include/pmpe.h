@@ -68,6 +68,14 @@ typedef enum { PMPE_F32 = 0, PMPE_BF16 = 1 } pmpe_dtype;
  * POOL_SOFTMAX  softmax over the whole permitted pool, gates not renormalised. */
 typedef enum { PMPE_GATE_RENORM_TOPK = 0, PMPE_GATE_POOL_SOFTMAX = 1 } pmpe_gate_mode;
 
+/* Routing mode. MASKED is the method: the policy mask is applied before top-k. SOFT is
+ * the paper's soft-routing control (Sec. 4.2, third row of the control matrix; App. E):
+ * one router over the concatenated public and private pool, no mask, for every token
+ * whatever its policy word. It exists to show what the mask prevents (deny tokens then
+ * reach private experts and the execution audit counts them as violations); it is not
+ * a safe configuration. */
+typedef enum { PMPE_ROUTE_MASKED = 0, PMPE_ROUTE_SOFT = 1 } pmpe_route_mode;
+
 /* Policy words. Exactly one 32-bit value allows; every other value - including
  * corrupted words - is malformed and resolves to deny (fail closed). */
 #define PMPE_POLICY_ALLOW 0xA11C0DE5u
@@ -94,6 +102,7 @@ typedef struct {
   int32_t act_dtype;    /* pmpe_dtype of x, x_perm, y_perm, y_shared, out */
   int32_t w_dtype;      /* pmpe_dtype of expert weights; must equal act_dtype */
   int32_t gate_mode;    /* pmpe_gate_mode */
+  int32_t route_mode;   /* pmpe_route_mode; 0 (zero-initialised) = MASKED */
 } pmpe_layer_desc;
 /* The expert kernels use 32-bit byte offsets, so validation also requires fewer than
  * 2^31 elements in: T*top_k*max(hidden, inter), T*hidden, T*n_shared*shared_inter,
@@ -123,7 +132,9 @@ pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T);
  * logit_bias[e], one fp32 add) are computed for the permitted pool ONLY: the other
  * pool's logits are never formed, and a deny token's x is never multiplied with
  * private router rows. The k largest logits win, equal fp32 values going to the
- * lower expert id (-0.0 == +0.0).
+ * lower expert id (-0.0 == +0.0). With route_mode SOFT (control arm only) every token
+ * ranks all n_pub + n_priv logits, wr_priv must not be NULL (else PMPE_ERR_NULL), and the
+ * allow output still reports the resolved policy decision.
  *
  *   x            [T, H] act_dtype
  *   wr_pub       [n_pub, H] fp32, frozen router rows

@@ -21,6 +21,9 @@ computes, following Policy-Masked Private Experts (arXiv 2608.06690):
              separate function that counts the rows it executes, like the
              independent forward hooks of App. F.1
 * combine    out_t = sum_j g_tj * y_{e_tj}(x_t) (+ shared experts)
+* soft       the soft-routing control of Sec. 4.2 (third row of the control matrix)
+             and App. E: one router over the concatenated public and private pool, no
+             mask; kept only to show what the mask prevents
 * audit      per-request private rows, deny violations (App. B.2 "route counters
              indexed by row and layer"; App. F.1)
 
@@ -164,9 +167,13 @@ class Route:
 
 
 def route(x: np.ndarray, wr_pub: np.ndarray, wr_priv: np.ndarray, bias: Optional[np.ndarray],
-          words: Sequence[int], k: int, gate_mode: str = GATE_RENORM) -> Route:
+          words: Sequence[int], k: int, gate_mode: str = GATE_RENORM, soft: bool = False) -> Route:
     """Masked top-k routing of every token. Private router rows are only ever read for
-    tokens whose word allows; an ineligible expert never enters the candidate set."""
+    tokens whose word allows; an ineligible expert never enters the candidate set.
+
+    soft=True is the control arm of Sec. 4.2 / App. E: every token ranks the logits of
+    the concatenated pool (public ids then private ids) with no mask; `allow` still
+    records the resolved policy decision."""
     x = np.asarray(x)
     T = x.shape[0]
     n_pub, n_priv = wr_pub.shape[0], wr_priv.shape[0] if wr_priv is not None else 0
@@ -176,6 +183,19 @@ def route(x: np.ndarray, wr_pub: np.ndarray, wr_priv: np.ndarray, bias: Optional
     gap = np.zeros(T, np.float64)
     zs: List[np.ndarray] = [None] * T  # type: ignore
     taus = np.array([decode_word(w) for w in words], dtype=np.int64)
+    if soft:
+        ids = np.arange(n_pub + n_priv)
+        wr = np.concatenate([np.asarray(wr_pub), np.asarray(wr_priv)], axis=0)
+        b = None if bias is None else np.asarray(bias, np.float32)
+        z = logits(x, wr, b)
+        for t in range(T):
+            sel, g = topk(z[t], ids, k)
+            idx[t] = sel
+            gate[t] = gates(z[t][sel], z[t], gate_mode)
+            allow[t] = taus[t]
+            gap[t] = g
+            zs[t] = z[t]
+        return Route(idx, gate, allow, gap, zs)
     for tau in (0, 1):
         toks = np.nonzero(taus == tau)[0]
         if len(toks) == 0:
@@ -281,7 +301,8 @@ class LayerResult:
 
 def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_priv, w2_priv,
                   words: Sequence[int], k: int, gate_mode: str = GATE_RENORM,
-                  w13_sh=None, w2_sh=None, tokens: Optional[Sequence[int]] = None) -> LayerResult:
+                  w13_sh=None, w2_sh=None, tokens: Optional[Sequence[int]] = None,
+                  soft: bool = False) -> LayerResult:
     """One policy-masked MoE layer. Routing and dispatch cover every token; expert
     outputs are evaluated for `tokens` (all by default). Weight containers are
     indexed by expert (e.g. w13_pub[e] -> [2I, H])."""
@@ -290,7 +311,7 @@ def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_pri
     n_pub = wr_pub.shape[0]
     n_priv = wr_priv.shape[0] if wr_priv is not None else 0
     E = n_pub + n_priv
-    rt = route(x, wr_pub, wr_priv, bias, words, k, gate_mode)
+    rt = route(x, wr_pub, wr_priv, bias, words, k, gate_mode, soft=soft)
     dp = dispatch(rt.idx, E)
     toks = np.arange(T) if tokens is None else np.asarray(tokens, np.int64)
     hook = ExecutionHook(T, n_priv)

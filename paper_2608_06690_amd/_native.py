@@ -29,6 +29,8 @@ PMPE_F32 = 0
 PMPE_BF16 = 1
 PMPE_GATE_RENORM_TOPK = 0
 PMPE_GATE_POOL_SOFTMAX = 1
+PMPE_ROUTE_MASKED = 0
+PMPE_ROUTE_SOFT = 1
 PMPE_POLICY_ALLOW = 0xA11C0DE5
 PMPE_POLICY_DENY = 0x00000000
 PMPE_DEV_PRIV_ROUTER_MISSING = 0x1
@@ -50,7 +52,7 @@ class PmpeError(RuntimeError):
 class LayerDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "hidden", "inter", "n_pub", "n_priv", "top_k", "n_shared", "shared_inter",
-        "act_dtype", "w_dtype", "gate_mode")]
+        "act_dtype", "w_dtype", "gate_mode", "route_mode")]
 
 
 _P = ctypes.c_void_p
@@ -86,10 +88,11 @@ def lib() -> ctypes.CDLL:
 
 
 def make_desc(hidden: int, inter: int, n_pub: int, n_priv: int, top_k: int, n_shared: int = 0,
-              shared_inter: int = 0, bf16: bool = True, gate_mode: int = PMPE_GATE_RENORM_TOPK
-              ) -> LayerDesc:
+              shared_inter: int = 0, bf16: bool = True, gate_mode: int = PMPE_GATE_RENORM_TOPK,
+              route_mode: int = 0) -> LayerDesc:
     dt = PMPE_BF16 if bf16 else PMPE_F32
-    return LayerDesc(hidden, inter, n_pub, n_priv, top_k, n_shared, shared_inter, dt, dt, gate_mode)
+    return LayerDesc(hidden, inter, n_pub, n_priv, top_k, n_shared, shared_inter, dt, dt, gate_mode,
+                     route_mode)
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:

@@ -34,6 +34,8 @@ pmpe_status check_desc(const pmpe_layer_desc* d, int32_t T) {
   }
   if (d->gate_mode != PMPE_GATE_RENORM_TOPK && d->gate_mode != PMPE_GATE_POOL_SOFTMAX)
     return PMPE_ERR_SHAPE;
+  if (d->route_mode != PMPE_ROUTE_MASKED && d->route_mode != PMPE_ROUTE_SOFT) return PMPE_ERR_SHAPE;
+  if (d->route_mode == PMPE_ROUTE_SOFT && d->n_pub + d->n_priv > 2 * PMPE_MAX_POOL) return PMPE_ERR_SHAPE;
   if ((int64_t)T * d->top_k > (int64_t)INT32_MAX / 2) return PMPE_ERR_SHAPE;
   // the expert kernels address rows of x, x_perm, h and of one expert's weights with
   // 32-bit byte offsets (bf16 elements, so fewer than 2^31 elements)
@@ -47,7 +49,11 @@ pmpe_status check_desc(const pmpe_layer_desc* d, int32_t T) {
   return PMPE_OK;
 }
 
-int route_zstride(const pmpe_layer_desc* d) { return d->n_pub > d->n_priv ? d->n_pub : d->n_priv; }
+// logits row: the permitted pool (masked), or the concatenated pool (soft control)
+int route_zstride(const pmpe_layer_desc* d) {
+  if (d->route_mode == PMPE_ROUTE_SOFT) return d->n_pub + d->n_priv;
+  return d->n_pub > d->n_priv ? d->n_pub : d->n_priv;
+}
 
 size_t route_ws(const pmpe_layer_desc* d, int32_t T) {
   return round_up((size_t)T * route_zstride(d) * 4);
@@ -107,9 +113,11 @@ pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const
   if (T == 0) return PMPE_OK;
   if (!ws || ws_bytes < route_ws(d, T)) return PMPE_ERR_WORKSPACE;
   if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  if (d->route_mode == PMPE_ROUTE_SOFT && !wr_priv) return PMPE_ERR_NULL;
   RouteArgs a{T, d->hidden, d->n_pub, d->n_priv, d->top_k, d->gate_mode,
               d->act_dtype == PMPE_BF16, x, wr_pub, wr_priv, logit_bias, policy_word,
-              topk_idx, topk_gate, allow, kgap, dev_status, (float*)ws, route_zstride(d)};
+              topk_idx, topk_gate, allow, kgap, dev_status, (float*)ws, route_zstride(d),
+              d->route_mode == PMPE_ROUTE_SOFT ? 1 : 0};
   return launched(launch_route(a, (hipStream_t)stream));
 }
 

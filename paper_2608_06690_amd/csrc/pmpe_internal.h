@@ -88,6 +88,7 @@ struct RouteArgs {
   uint32_t* dev_status;
   float* z;     // workspace [T, zstride]: fp32 logits of each token's permitted pool
   int zstride;
+  int soft;     // control arm: every token ranks the concatenated pool (z holds all E logits)
 };
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 

@@ -101,11 +101,10 @@ struct TopkCtx {
   float* kgap;
 };
 
+// Top-k of token t over its pool: N logits z[0..N) of expert ids base + s.
 template <int NPL>
-__device__ void topk_one_token(const TopkCtx& c, int t, int tau, const float* z) {
+__device__ void topk_one_token(const TopkCtx& c, int t, int tau, int N, int base, const float* z) {
   const int lane = lane_id();
-  const int N = tau ? c.n_priv : c.n_pub;
-  const int base = tau ? c.n_pub : 0;
   const int k = c.k;
   uint64_t key[NPL];
 #pragma unroll
@@ -185,7 +184,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   if (tid < TT) {
     const int tau = (t0 + tid < a.T) ? token_tau(a, t0 + tid) : -1;
     s_tau[tid] = tau;
-    mine = (tau == pass) ? 1 : 0;
+    mine = (a.soft ? tau >= 0 : tau == pass) ? 1 : 0;
     if (mine) atomicMin(&s_first, tid);
   }
   // no token of this pool's policy in the tile: its router rows are never read
@@ -196,7 +195,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   // Operand rows of this lane. A lane whose expert is past the pool, or whose token
   // has the other policy, reads a row that belongs to this pass (expert n0, the
   // tile's first token of this policy) and its results are discarded: a token's x
-  // is only ever loaded for the pool its policy permits.
+  // is only ever loaded for the pool its policy permits (in the soft control arm every
+  // token takes part in both pools).
   const int n = n0 + (lane & 15);
   const int koff = (lane >> 4) * 8;
   const float* wrow = wr + (size_t)(n < N ? n : n0) * H + koff;
@@ -205,7 +205,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb) {
     const int tt = mb * 16 + (lane & 15);
-    xrow[mb] = x + (size_t)(t0 + (s_tau[tt] == pass ? tt : first)) * H + koff;
+    const bool part = a.soft ? s_tau[tt] >= 0 : s_tau[tt] == pass;
+    xrow[mb] = x + (size_t)(t0 + (part ? tt : first)) * H + koff;
   }
   const int nsteps = H / (32 * RT_WAVES);  // K steps of this wave's quarter
   const int kbase = wave * nsteps;
@@ -270,12 +271,12 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   for (int o = tid; o < TT * 16; o += RT_THREADS) {
     const int tt = o >> 4, c = o & 15;
     const int nn = n0 + c;
-    if (s_tau[tt] != pass || nn >= N) continue;
+    if ((a.soft ? s_tau[tt] < 0 : s_tau[tt] != pass) || nn >= N) continue;
     float z = s_part[0][tt][c];
 #pragma unroll
     for (int w2 = 1; w2 < RT_WAVES; ++w2) z += s_part[w2][tt][c];
     if (a.bias) z += a.bias[(pass ? a.n_pub : 0) + nn];
-    a.z[(size_t)(t0 + tt) * a.zstride + nn] = z;
+    a.z[(size_t)(t0 + tt) * a.zstride + (a.soft && pass ? a.n_pub : 0) + nn] = z;
   }
 }
 
@@ -284,18 +285,20 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
 __global__ __launch_bounds__(RT_THREADS) void route_logits_f32_kernel(RouteArgs a) {
   const int t = blockIdx.x;
   const int tau = token_tau(a, t);
-  const int N = tau ? a.n_priv : a.n_pub;
-  const float* wr = tau ? a.wr_priv : a.wr_pub;
+  // masked: the permitted pool; soft (control arm): public then private rows
+  const int N = a.soft ? a.n_pub + a.n_priv : (tau ? a.n_priv : a.n_pub);
+  const int base = (a.soft || !tau) ? 0 : a.n_pub;
   const float* xr = (const float*)a.x + (size_t)t * a.H;
   for (int n = threadIdx.x; n < N; n += RT_THREADS) {
-    const float* wrow = wr + (size_t)n * a.H;
+    const int e = base + n;  // global expert id
+    const float* wrow = (e < a.n_pub) ? a.wr_pub + (size_t)e * a.H : a.wr_priv + (size_t)(e - a.n_pub) * a.H;
     float acc = 0.0f;
     for (int h0 = 0; h0 < a.H; h0 += 64) {
       float part = 0.0f;
       for (int h = h0; h < h0 + 64; ++h) part = fmaf(xr[h], wrow[h], part);
       acc += part;
     }
-    if (a.bias) acc += a.bias[(tau ? a.n_pub : 0) + n];
+    if (a.bias) acc += a.bias[e];
     a.z[(size_t)t * a.zstride + n] = acc;
   }
 }
@@ -305,15 +308,19 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
   const int t = blockIdx.x * RT_WAVES + (threadIdx.x >> 6);
   if (t >= a.T) return;
   const int tau = token_tau(a, t);
-  const int N = tau ? a.n_priv : a.n_pub;
+  // masked: the permitted pool; soft (control arm): the concatenated pool
+  const int N = a.soft ? a.n_pub + a.n_priv : (tau ? a.n_priv : a.n_pub);
+  const int base = (a.soft || !tau) ? 0 : a.n_pub;
   const float* z = a.z + (size_t)t * a.zstride;
   TopkCtx c{a.T, a.n_pub, a.n_priv, a.k, a.gate_mode, a.topk_idx, a.topk_gate, a.allow, a.kgap};
   if (N <= 64)
-    topk_one_token<1>(c, t, tau, z);
+    topk_one_token<1>(c, t, tau, N, base, z);
   else if (N <= 128)
-    topk_one_token<2>(c, t, tau, z);
+    topk_one_token<2>(c, t, tau, N, base, z);
+  else if (N <= 256)
+    topk_one_token<4>(c, t, tau, N, base, z);
   else
-    topk_one_token<4>(c, t, tau, z);
+    topk_one_token<8>(c, t, tau, N, base, z);
 }
 
 }  // namespace

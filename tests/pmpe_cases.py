@@ -64,25 +64,26 @@ def oracle_inputs(cfg: W.LayerConfig, layer: int = 0, x: Optional[torch.Tensor] 
 
 
 def oracle_layer(cfg: W.LayerConfig, oi: OracleInputs, words: Sequence[int],
-                 tokens: Optional[Sequence[int]] = None) -> O.LayerResult:
+                 tokens: Optional[Sequence[int]] = None, soft: bool = False) -> O.LayerResult:
     return O.layer_forward(oi.x, oi.wr_pub, oi.wr_priv, oi.bias, oi.w13_pub, oi.w2_pub,
                            oi.w13_priv, oi.w2_priv, words, cfg.top_k, cfg.gate_mode,
-                           oi.w13_sh, oi.w2_sh, tokens)
+                           oi.w13_sh, oi.w2_sh, tokens, soft=soft)
 
 
-def make_desc(cfg: W.LayerConfig):
+def make_desc(cfg: W.LayerConfig, soft: bool = False):
     import paper_2608_06690_amd as P
     gm = P.PMPE_GATE_POOL_SOFTMAX if cfg.gate_mode == "pool_softmax" else P.PMPE_GATE_RENORM_TOPK
     return P.make_desc(cfg.hidden, cfg.inter, cfg.n_pub, cfg.n_priv, cfg.top_k, cfg.n_shared,
-                       cfg.shared_inter, cfg.dtype == "bf16", gm)
+                       cfg.shared_inter, cfg.dtype == "bf16", gm,
+                       P.PMPE_ROUTE_SOFT if soft else P.PMPE_ROUTE_MASKED)
 
 
 def device_layer(cfg: W.LayerConfig, layer: int = 0, device="cuda", gather_in_dispatch=False,
-                 drop_private: bool = False):
+                 drop_private: bool = False, soft: bool = False):
     import paper_2608_06690_amd as P
     Lw = W.make_layer(cfg, layer, device)
     priv = (lambda t: None) if drop_private else (lambda t: t)
-    return P.PolicyMaskedMoE(make_desc(cfg), Lw.wr_pub, priv(Lw.wr_priv), Lw.bias, Lw.w13_pub,
+    return P.PolicyMaskedMoE(make_desc(cfg, soft), Lw.wr_pub, priv(Lw.wr_priv), Lw.bias, Lw.w13_pub,
                              Lw.w2_pub, priv(Lw.w13_priv), priv(Lw.w2_priv), Lw.w13_sh, Lw.w2_sh,
                              gather_in_dispatch=gather_in_dispatch), Lw
 

@@ -49,6 +49,14 @@ def desc(**kw):
     return P.make_desc(**base)
 
 
+def test_package_exports_descriptor_constants():
+    for name in ["PMPE_BF16", "PMPE_F32", "PMPE_GATE_RENORM_TOPK", "PMPE_GATE_POOL_SOFTMAX",
+                 "PMPE_ROUTE_MASKED", "PMPE_ROUTE_SOFT", "PMPE_POLICY_ALLOW", "PMPE_POLICY_DENY"]:
+        assert hasattr(P, name), name
+    d = P.make_desc(128, 64, 8, 8, 2, route_mode=P.PMPE_ROUTE_SOFT)
+    assert d.route_mode == 1 and P.make_desc(128, 64, 8, 8, 2).route_mode == 0
+
+
 def test_valid_descriptor_and_workspace():
     d = desc()
     assert P.pmpe_check_desc(d, 4096) == 0
@@ -81,6 +89,11 @@ def test_dtype_and_gate_mode_codes():
     d = desc()
     d.gate_mode = 5
     assert P.pmpe_check_desc(d, 16) == -2
+    d = desc()
+    d.route_mode = 2
+    assert P.pmpe_check_desc(d, 16) == -2
+    d.route_mode = N.PMPE_ROUTE_SOFT
+    assert P.pmpe_check_desc(d, 16) == 0
     assert P.pmpe_check_desc(desc(), -1) == -2
     # 32-bit byte offsets of the permuted rows: T*k*max(H, I) must stay below 2^31
     assert P.pmpe_check_desc(desc(hidden=8192, top_k=8), 32768) == -2
@@ -113,6 +126,12 @@ def test_null_and_alignment_rejected_before_launch():
     st = lib.pmpe_route(ctypes.byref(d), 16, 0x1004, 0x1000, None, None, None, 0x2000, 0x3000,
                         0x4000, None, None, 0x5000, 1 << 20, None)
     assert st == -5
+    # soft-routing control without the private router rows
+    ds = desc()
+    ds.route_mode = N.PMPE_ROUTE_SOFT
+    st = lib.pmpe_route(ctypes.byref(ds), 16, 0x1000, 0x1000, None, None, None, 0x2000, 0x3000,
+                        0x4000, None, None, 0x5000, 1 << 20, None)
+    assert st == -1
     # dispatch without workspace
     st = lib.pmpe_dispatch(ctypes.byref(d), 16, 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000,
                            None, None, 0, None)

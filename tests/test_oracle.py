@@ -320,6 +320,53 @@ def test_all_allow_equals_private_only_moe():
     assert np.allclose(res.out[ok], ref[ok], rtol=1e-6, atol=1e-12)  # gates are fp32
 
 
+# ----------------------------------------------------------------------------
+# Soft-routing control (Sec. 4.2, third row of the control matrix; App. E)
+# ----------------------------------------------------------------------------
+
+def run_soft(cfg, L, x, words, bias=None, soft=True):
+    return O.layer_forward(
+        x, np64(L.wr_pub), np64(L.wr_priv), bias, np64(L.w13_pub), np64(L.w2_pub),
+        np64(L.w13_priv), np64(L.w2_priv), words, cfg.top_k, cfg.gate_mode, soft=soft)
+
+
+def test_soft_router_equals_textbook_concatenated_moe():
+    """The control arm ignores the policy: every token gets the plain top-k MoE over the
+    concatenated pool (public rows then private rows), whatever its word."""
+    cfg, L, x, req, words = tiny_case()
+    res = run_soft(cfg, L, x, words)
+    ok = ~res.route.near_tie
+    assert ok.sum() >= cfg.tokens - 3
+    wr = np.concatenate([np64(L.wr_pub), np64(L.wr_priv)])
+    w13 = np.concatenate([np64(L.w13_pub), np64(L.w13_priv)])
+    w2 = np.concatenate([np64(L.w2_pub), np64(L.w2_priv)])
+    ref = textbook_public_moe(x, wr, w13, w2, cfg.top_k)
+    assert np.allclose(res.out[ok], ref[ok], rtol=1e-6, atol=1e-12)
+    # the route log still records the resolved policy decision
+    assert np.array_equal(res.route.allow, np.array([O.decode_word(w) for w in words], np.uint8))
+
+
+def test_soft_router_leaks_to_deny_and_the_audit_counts_it():
+    """With a logit bias that favours the private experts, soft routing sends deny tokens
+    to private experts; the execution audit reports every such token as a violation,
+    while the masked route of the same inputs executes no private row for them (a bias
+    shared by a whole pool does not change the masked selection)."""
+    cfg, L, x, req, words = tiny_case()
+    bias = np.concatenate([np.zeros(cfg.n_pub), np.full(cfg.n_priv, 100.0)]).astype(np.float32)
+    soft = run_soft(cfg, L, x, words, bias)
+    masked = run_soft(cfg, L, x, words, bias, soft=False)
+    taus = np.array([O.decode_word(w) for w in words])
+    deny = taus == 0
+    assert deny.sum() > 0
+    # every selected expert is private for every token under the soft router
+    assert np.all(soft.route.idx >= cfg.n_pub)
+    assert np.array_equal(soft.hook.rows, np.full(cfg.tokens, cfg.top_k))
+    a_soft = O.audit(soft.hook.rows, soft.route.allow, req.offsets)
+    a_mask = O.audit(masked.hook.rows, masked.route.allow, req.offsets)
+    assert a_soft.deny_violations == int(deny.sum())
+    assert a_mask.deny_violations == 0 and np.all(masked.hook.rows[deny] == 0)
+
+
 def test_shared_experts_add_dense_swiglu():
     cfg = W.scaled_config(W.get_config("deepseek"), tokens=24, requests=2, hidden=64, inter=32,
                           n_pub=6, n_priv=4, top_k=2, shared_inter=16)
