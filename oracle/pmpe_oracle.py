@@ -364,3 +364,30 @@ def audit(token_rows: np.ndarray, allow: np.ndarray, req_offset: Sequence[int]) 
         req[r] = int(token_rows[req_offset[r]:req_offset[r + 1]].sum())
     viol = int(((np.asarray(allow) == 0) & (token_rows > 0)).sum())
     return Audit(req, int(req.sum()), viol)
+
+
+# ----------------------------------------------------------------------------
+# Public-weight fingerprint: the frozen public weights are hashed before and after
+# training and must be unchanged (Sec. 3.2 training and checkpointing; Sec. 5.1; App. C.1)
+# ----------------------------------------------------------------------------
+
+FP_LEAF = 1024     # bytes per leaf chunk
+FP_FANOUT = 16     # child digests hashed together per inner node
+
+
+def fingerprint(data: bytes) -> bytes:
+    """16-ary SHA-256 tree over a byte string.
+
+    Level 0: the SHA-256 digest of every 1024-byte chunk (the last chunk may be short;
+    an empty input is one empty chunk). Level j+1: the SHA-256 digest of the
+    concatenation of up to 16 consecutive level-j digests. The root, when one digest
+    remains, is the fingerprint (an input of at most 1024 bytes has root SHA-256(data)).
+    SHA-256 itself is FIPS 180-4, taken from hashlib."""
+    import hashlib
+    data = bytes(data)
+    n = max(1, -(-len(data) // FP_LEAF))
+    level = [hashlib.sha256(data[i * FP_LEAF:(i + 1) * FP_LEAF]).digest() for i in range(n)]
+    while len(level) > 1:
+        level = [hashlib.sha256(b"".join(level[i:i + FP_FANOUT])).digest()
+                 for i in range(0, len(level), FP_FANOUT)]
+    return level[0]

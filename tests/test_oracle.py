@@ -476,3 +476,46 @@ def test_generator_slices_and_moments():
     assert torch.equal(a, L.w13_pub[3])
     v = W.normal(W.tensor_key(1, 2, 3), (200000,), 0.5)
     assert abs(float(v.mean())) < 0.01 and abs(float(v.std()) - 0.5) < 0.01
+
+
+# ----------------------------------------------------------------------------
+# Fingerprint tree (SHA-256 from FIPS 180-4; published example digests)
+# ----------------------------------------------------------------------------
+
+FIPS_EXAMPLES = {
+    b"abc": "ba7816bf8f01cfea414140de5dae2223b00361a396177a9cb410ff61f20015ad",
+    b"": "e3b0c44298fc1c149afbf4c8996fb92427ae41e4649b934ca495991b7852b855",
+    b"abcdbcdecdefdefgefghfghighijhijkijkljklmklmnlmnomnopnopq":
+        "248d6a61d20638b8e5c026930c3e6039a33ce45964ff2167f6ecedd419db06c1",
+}
+
+
+def test_fingerprint_single_leaf_is_sha256_of_the_input():
+    for msg, hexd in FIPS_EXAMPLES.items():
+        assert O.fingerprint(msg).hex() == hexd
+
+
+def test_fingerprint_tree_closed_forms():
+    import hashlib
+    h = lambda b: hashlib.sha256(b).digest()  # noqa: E731
+    rng = np.random.default_rng(5)
+    data = rng.integers(0, 256, 1024 * 3 + 17, dtype=np.uint8).tobytes()
+    # one leaf
+    assert O.fingerprint(data[:1024]) == h(data[:1024])
+    # four leaves, one inner node
+    leaves = b"".join(h(data[i:i + 1024]) for i in range(0, len(data), 1024))
+    assert O.fingerprint(data) == h(leaves)
+    # 17 leaves: two inner nodes (16 + 1), then the root over their two digests
+    big = bytes(1024 * 16) + b"x"
+    inner0 = h(b"".join([h(bytes(1024))] * 16))
+    inner1 = h(h(b"x"))
+    assert O.fingerprint(big) == h(inner0 + inner1)
+    # 16 * 16 + 1 leaves: three levels above the leaves
+    big = bytes(1024 * 257)
+    l1 = [h(b"".join([h(bytes(1024))] * 16))] * 16 + [h(h(bytes(1024)))]
+    l2 = [h(b"".join(l1[:16])), h(l1[16])]
+    assert O.fingerprint(big) == h(b"".join(l2))
+    # any changed byte changes the root
+    flipped = bytearray(data)
+    flipped[5000] ^= 1
+    assert O.fingerprint(bytes(flipped)) != O.fingerprint(data)
