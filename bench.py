@@ -29,6 +29,12 @@ if ROOT not in sys.path:
 METRIC = "MoE-layer tokens/s (Qwen3-30B-A3B shape) + % MFMA peak; decode % HBM BW"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+# Integer VALU rate: 256 CUs x 64 lanes x 2.4 GHz, one 32-bit operation per lane per clock.
+PEAK_VALU_OPS = 256 * 64 * 2.4e9
+# SHA-256 needs about 1400 such operations per 64-byte block on CDNA4 (rotations and the
+# two 3-input logic functions take one operation each, three-way xors and sums one each):
+# 64 rounds x 14, 48 schedule words x 10, 8 state sums, 16 byte swaps.
+SHA256_OPS_PER_BLOCK = 64 * 14 + 48 * 10 + 8 + 16
 CALLS = ["route", "dispatch", "expert_ffn", "combine", "audit"]
 COPY_BYTES = 1 << 30
 
@@ -55,6 +61,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true")
+    p.add_argument("--no-fingerprint", action="store_true")
+    p.add_argument("--fingerprint-only", action="store_true",
+                   help="only time the public-weight fingerprint")
     p.add_argument("--cpu-sample", type=int, default=4096, help="tokens in the CPU-oracle sample")
     p.add_argument("--cpu-reps", type=int, default=3, help="timed repetitions of the CPU oracle")
     p.add_argument("--decode-only", action="store_true",
@@ -227,6 +236,36 @@ def decode_bench(args, dev):
     return res
 
 
+def fingerprint_bench(args, dev):
+    """Fingerprint of one Qwen-shaped layer's public expert weights (w13 and w2, bf16):
+    per-call time and the rate against the integer-VALU bound of SHA-256."""
+    import torch
+    import workloads as W
+    import paper_2608_06690_amd as P
+    cfg = W.get_config("qwen")
+    Lw = W.make_layer(cfg, 0, dev)
+    bufs = [Lw.w13_pub, Lw.w2_pub]
+    nbytes = sum(t.numel() * t.element_size() for t in bufs)
+    for _ in range(max(1, args.warmup // 2)):
+        P.fingerprint_tensors(*bufs)
+    torch.cuda.synchronize()
+    reps = max(3, args.steps // 5)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        P.fingerprint_tensors(*bufs)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    gbs = nbytes / (us * 1e-6) / 1e9
+    peak_gbs = PEAK_VALU_OPS / (SHA256_OPS_PER_BLOCK / 64) / 1e9
+    del Lw, bufs
+    torch.cuda.empty_cache()
+    return {"workload": "public expert weights of one qwen3-30b-a3b-shaped layer (w13 + w2, bf16)",
+            "bytes": nbytes, "us_per_call": us, "gbs": gbs, "bound": "alu",
+            "peak_gbs": peak_gbs, "frac": gbs / peak_gbs, "reps": reps}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -254,6 +293,9 @@ def main():
         return
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
+        return
+    if args.fingerprint_only:
+        print(json.dumps(fingerprint_bench(args, dev)), flush=True)
         return
     if args.all_deny:
         cfg, layer, x, words, req_off, audit, bufs, req = setup("qwen", dev, all_deny=True,
@@ -303,6 +345,8 @@ def main():
 
     if not args.no_decode:
         out["decode"] = decode_bench(args, dev)
+    if not args.no_fingerprint:
+        out["fingerprint"] = fingerprint_bench(args, dev)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, req, args.cpu_sample, args.cpu_reps)

@@ -255,6 +255,40 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
                        uint64_t* req_private_rows, uint64_t* total_private_rows,
                        uint32_t* deny_violations, pmpe_stream_t stream);
 
+/*
+ * pmpe_fingerprint - SHA-256 tree digest of a device buffer, to show that the frozen
+ * public weights are unchanged (hashed before and after training and after a reload,
+ * Sec. 3.2 training and checkpointing, Sec. 5.1, App. C.1).
+ *
+ * Definition: level 0 is the SHA-256 digest (FIPS 180-4) of every PMPE_FP_LEAF_BYTES
+ * chunk of the buffer, in order (the last chunk may be short; an empty buffer is one
+ * empty chunk). Level j+1 is the SHA-256 digest of the concatenation of each run of up
+ * to PMPE_FP_FANOUT consecutive level-j digests. The fingerprint is the single digest
+ * of the first level that has one; a buffer of at most PMPE_FP_LEAF_BYTES bytes thus
+ * has SHA-256(buffer) as its fingerprint. A set of tensors is fingerprinted by
+ * fingerprinting the concatenation of their fingerprints.
+ *
+ *   data     device, nbytes bytes, any alignment (16-byte aligned data loads whole
+ *            64-byte blocks as vectors; other data is read byte by byte, more slowly);
+ *            may be NULL only when nbytes == 0
+ *   nbytes   0 .. PMPE_FP_MAX_BYTES
+ *   digest   device, 32 bytes out, 16-byte aligned: the digest bytes in standard order
+ *   ws       device workspace of pmpe_fingerprint_workspace_bytes(nbytes) bytes,
+ *            16-byte aligned; may be NULL when that size is 0
+ *
+ * Errors: PMPE_ERR_NULL (data with nbytes > 0, or digest, or a needed ws is NULL),
+ * PMPE_ERR_SHAPE (nbytes too large), PMPE_ERR_ALIGN (digest or ws), PMPE_ERR_WORKSPACE.
+ * The call is asynchronous on `stream`; data must not change until it has completed.
+ */
+#define PMPE_FP_LEAF_BYTES 1024
+#define PMPE_FP_FANOUT 16
+#define PMPE_FP_MAX_BYTES ((uint64_t)1 << 46)
+
+size_t pmpe_fingerprint_workspace_bytes(uint64_t nbytes);
+
+pmpe_status pmpe_fingerprint(const void* data, uint64_t nbytes, uint8_t* digest, void* ws,
+                             size_t ws_bytes, pmpe_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

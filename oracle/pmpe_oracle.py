@@ -391,3 +391,9 @@ def fingerprint(data: bytes) -> bytes:
         level = [hashlib.sha256(b"".join(level[i:i + FP_FANOUT])).digest()
                  for i in range(0, len(level), FP_FANOUT)]
     return level[0]
+
+
+def fingerprint_set(parts: Sequence[bytes]) -> bytes:
+    """Fingerprint of several buffers: the fingerprint of the concatenation of their
+    fingerprints, in order."""
+    return fingerprint(b"".join(fingerprint(p) for p in parts))

@@ -4,7 +4,9 @@ The computation lives in libpmpe.so (HIP kernels for gfx950 behind the C ABI of
 include/pmpe.h); this package is its binding."""
 from ._native import (PMPE_BF16, PMPE_F32, PMPE_GATE_POOL_SOFTMAX, PMPE_GATE_RENORM_TOPK,  # noqa: F401
                       PMPE_POLICY_ALLOW, PMPE_POLICY_DENY, PMPE_ROUTE_MASKED, PMPE_ROUTE_SOFT,
-                      LayerDesc, PmpeError, make_desc,
+                      PMPE_FP_FANOUT, PMPE_FP_LEAF_BYTES, LayerDesc, PmpeError,
+                      fingerprint_tensors, make_desc, pmpe_fingerprint,
+                      pmpe_fingerprint_workspace_bytes,
                       pmpe_audit, pmpe_check_desc, pmpe_combine, pmpe_dispatch, pmpe_expert_ffn,
                       pmpe_route, pmpe_version, pmpe_workspace_bytes)
 from .layer import AuditBuffers, LayerBuffers, PolicyMaskedMoE  # noqa: F401

@@ -79,8 +79,17 @@ _lib.pmpe_combine.argtypes = [_DESC, _I32] + [_P] * 5 + [_P]
 _lib.pmpe_audit.restype = _I32
 _lib.pmpe_audit.argtypes = [_DESC, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]
 
+_lib.pmpe_fingerprint_workspace_bytes.restype = _SZ
+_lib.pmpe_fingerprint_workspace_bytes.argtypes = [ctypes.c_uint64]
+_lib.pmpe_fingerprint.restype = _I32
+_lib.pmpe_fingerprint.argtypes = [_P, ctypes.c_uint64, _P, _P, _SZ, _P]
+
 EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_check_desc",
-            "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit"]
+            "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
+            "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint"]
+
+PMPE_FP_LEAF_BYTES = 1024
+PMPE_FP_FANOUT = 16
 
 
 def lib() -> ctypes.CDLL:
@@ -164,3 +173,35 @@ def pmpe_audit(desc, T, audit_token_rows, allow, req_offset, R, req_private_rows
     _check(_lib.pmpe_audit(ctypes.byref(desc), T, _ptr(audit_token_rows), _ptr(allow),
                            _ptr(req_offset), R, _ptr(req_private_rows), _ptr(total_private_rows),
                            _ptr(deny_violations), _stream(stream)), "pmpe_audit")
+
+
+def pmpe_fingerprint_workspace_bytes(nbytes: int) -> int:
+    return int(_lib.pmpe_fingerprint_workspace_bytes(nbytes))
+
+
+def pmpe_fingerprint(data: Optional[torch.Tensor], digest: torch.Tensor, ws: Optional[torch.Tensor],
+                     nbytes: Optional[int] = None, stream=None) -> None:
+    """Fingerprint the bytes of `data` (all of them unless `nbytes` is given) into the
+    32-byte device tensor `digest`."""
+    if nbytes is None:
+        nbytes = 0 if data is None else data.numel() * data.element_size()
+    _check(_lib.pmpe_fingerprint(_ptr(data), nbytes, _ptr(digest), _ptr(ws),
+                                 0 if ws is None else ws.numel() * ws.element_size(),
+                                 _stream(stream)), "pmpe_fingerprint")
+
+
+def fingerprint_tensors(*tensors: torch.Tensor, stream=None) -> torch.Tensor:
+    """One fingerprint of several device tensors: the fingerprint of the concatenation of
+    their fingerprints, in argument order. Returns a 32-byte uint8 device tensor."""
+    if not tensors:
+        raise ValueError("fingerprint_tensors needs at least one tensor")
+    dev = tensors[0].device
+    digests = torch.empty((len(tensors), 32), dtype=torch.uint8, device=dev)
+    ws_bytes = max(pmpe_fingerprint_workspace_bytes(t.numel() * t.element_size()) for t in tensors)
+    ws_bytes = max(ws_bytes, pmpe_fingerprint_workspace_bytes(32 * len(tensors)))
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    for i, t in enumerate(tensors):
+        pmpe_fingerprint(t, digests[i], ws, stream=stream)
+    root = torch.empty(32, dtype=torch.uint8, device=dev)
+    pmpe_fingerprint(digests, root, ws, stream=stream)
+    return root

@@ -72,6 +72,17 @@ size_t ffn_ws(const pmpe_layer_desc* d, int32_t T) {
 
 pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR_LAUNCH; }
 
+// two ping-pong digest arrays: every level fits in the one it does not read
+size_t fingerprint_ws_parts(uint64_t nbytes, size_t* part0) {
+  const uint64_t n = fingerprint_leaves(nbytes);
+  if (n <= 1) {
+    *part0 = 0;
+    return 0;
+  }
+  *part0 = round_up((size_t)n * 32);
+  return *part0 + round_up((size_t)((n + kFpFanout - 1) / kFpFanout) * 32);
+}
+
 }  // namespace
 
 extern "C" {
@@ -200,6 +211,28 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
   AuditArgs a{T, R, audit_token_rows, allow, req_offset, req_private_rows, total_private_rows,
               deny_violations};
   return launched(launch_audit(a, (hipStream_t)stream));
+}
+
+size_t pmpe_fingerprint_workspace_bytes(uint64_t nbytes) {
+  if (nbytes > PMPE_FP_MAX_BYTES) return 0;
+  size_t p0;
+  return fingerprint_ws_parts(nbytes, &p0);
+}
+
+pmpe_status pmpe_fingerprint(const void* data, uint64_t nbytes, uint8_t* digest, void* ws,
+                             size_t ws_bytes, pmpe_stream_t stream) {
+  if (nbytes > PMPE_FP_MAX_BYTES) return PMPE_ERR_SHAPE;
+  if (!digest || (nbytes > 0 && !data)) return PMPE_ERR_NULL;
+  if (!aligned16(digest)) return PMPE_ERR_ALIGN;
+  size_t p0;
+  const size_t need = fingerprint_ws_parts(nbytes, &p0);
+  if (need > 0) {
+    if (!ws) return PMPE_ERR_NULL;
+    if (ws_bytes < need) return PMPE_ERR_WORKSPACE;
+    if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  }
+  FingerprintArgs a{data, nbytes, digest, (uint8_t*)ws, need > 0 ? (uint8_t*)ws + p0 : nullptr};
+  return launched(launch_fingerprint(a, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -152,4 +152,19 @@ struct AuditArgs {
 };
 hipError_t launch_audit(const AuditArgs& a, hipStream_t s);
 
+// Fingerprint tree: 1 KiB leaves, 16 digests per inner node.
+constexpr uint32_t kFpLeafBytes = 1024;
+constexpr uint32_t kFpFanout = 16;
+
+struct FingerprintArgs {
+  const void* data;
+  uint64_t nbytes;
+  uint8_t* digest;  // 32 bytes out
+  uint8_t* ws;      // >= 32 * leaves bytes (unused when there is one leaf)
+  uint8_t* ws2;     // >= 32 * ceil(leaves / 16) bytes
+};
+
+uint64_t fingerprint_leaves(uint64_t nbytes);
+hipError_t launch_fingerprint(const FingerprintArgs& a, hipStream_t s);
+
 }  // namespace pmpe

@@ -26,7 +26,8 @@ def declarations():
 def test_header_declares_the_five_calls():
     d = declarations()
     for name in ["pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
-                 "pmpe_workspace_bytes", "pmpe_status_string", "pmpe_version", "pmpe_check_desc"]:
+                 "pmpe_workspace_bytes", "pmpe_status_string", "pmpe_version", "pmpe_check_desc",
+                 "pmpe_fingerprint", "pmpe_fingerprint_workspace_bytes"]:
         assert name in d, name
 
 
@@ -148,6 +149,26 @@ def test_null_and_alignment_rejected_before_launch():
     # audit: negative request count
     st = lib.pmpe_audit(ctypes.byref(d), 16, 0x1000, 0x2000, 0x3000, -1, 0x4000, 0x5000, 0x6000, None)
     assert st == -2
+
+
+def test_fingerprint_workspace_and_validation():
+    lib = N.lib()
+    ws = P.pmpe_fingerprint_workspace_bytes
+    # one leaf needs no workspace; n leaves need 32 n plus 32 ceil(n / 16), each rounded to 256
+    assert ws(0) == 0 and ws(1) == 0 and ws(1024) == 0
+    assert ws(1025) == 256 + 256
+    n = 3 * 1024 * 1024 // 1024
+    assert ws(3 * 1024 * 1024) == -(-32 * n // 256) * 256 + -(-32 * (-(-n // 16)) // 256) * 256
+    assert ws((1 << 46) + 1) == 0
+    assert P.PMPE_FP_LEAF_BYTES == 1024 and P.PMPE_FP_FANOUT == 16
+    # NULL digest, NULL data with bytes, too large, misaligned digest, missing/short workspace
+    assert lib.pmpe_fingerprint(0x1000, 16, None, None, 0, None) == -1
+    assert lib.pmpe_fingerprint(None, 16, 0x2000, None, 0, None) == -1
+    assert lib.pmpe_fingerprint(0x1000, (1 << 46) + 1, 0x2000, None, 0, None) == -2
+    assert lib.pmpe_fingerprint(0x1000, 16, 0x2008, None, 0, None) == -5
+    assert lib.pmpe_fingerprint(0x1000, 4096, 0x2000, None, 0, None) == -1
+    assert lib.pmpe_fingerprint(0x1000, 4096, 0x2000, 0x3000, 16, None) == -6
+    assert lib.pmpe_fingerprint(0x1000, 4096, 0x2000, 0x3008, 1 << 20, None) == -5
 
 
 def test_zero_tokens_launch_nothing():

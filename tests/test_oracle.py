@@ -519,3 +519,11 @@ def test_fingerprint_tree_closed_forms():
     flipped = bytearray(data)
     flipped[2000] ^= 1
     assert O.fingerprint(bytes(flipped)) != O.fingerprint(data)
+
+
+def test_fingerprint_set_of_small_buffers_is_hash_of_hashes():
+    import hashlib
+    h = lambda b: hashlib.sha256(b).digest()  # noqa: E731
+    parts = [b"abc", b"", bytes(range(200))]
+    assert O.fingerprint_set(parts) == h(h(b"abc") + h(b"") + h(bytes(range(200))))
+    assert O.fingerprint_set(parts) != O.fingerprint_set(parts[::-1])
