@@ -62,6 +62,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true")
     p.add_argument("--no-fingerprint", action="store_true")
+    p.add_argument("--vendor-gemm", action="store_true",
+                   help="only time hipBLASLt on the same expert GEMM shapes (context)")
     p.add_argument("--fingerprint-only", action="store_true",
                    help="only time the public-weight fingerprint")
     p.add_argument("--cpu-sample", type=int, default=4096, help="tokens in the CPU-oracle sample")
@@ -266,6 +268,49 @@ def fingerprint_bench(args, dev):
             "peak_gbs": peak_gbs, "frac": gbs / peak_gbs, "reps": reps}
 
 
+def vendor_gemm_bench(dev, reps=20):
+    """Context only: hipBLASLt (torch.bmm) on the Qwen layer's per-expert GEMM shapes with
+    uniform rows (128 per public expert, 512 per private expert), without the SwiGLU, the
+    row gather, the ragged expert sizes or the audit that the expert FFN kernel fuses in.
+    Both weight layouts are timed; the faster one counts."""
+    import torch
+    H, I = 2048, 768
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    g = torch.Generator(device=dev).manual_seed(1)
+    res = {}
+    for name, E, R in (("public", 128, 128), ("private", 32, 512)):
+        x = torch.randn(E, R, H, device=dev, dtype=torch.bfloat16, generator=g)
+        hh = torch.randn(E, R, I, device=dev, dtype=torch.bfloat16, generator=g)
+        w13 = torch.randn(E, H, 2 * I, device=dev, dtype=torch.bfloat16, generator=g)
+        w2 = torch.randn(E, I, H, device=dev, dtype=torch.bfloat16, generator=g)
+        w13t, w2t = w13.transpose(1, 2).contiguous(), w2.transpose(1, 2).contiguous()
+        o1 = torch.empty(E, R, 2 * I, device=dev, dtype=torch.bfloat16)
+        o2 = torch.empty(E, R, H, device=dev, dtype=torch.bfloat16)
+        g1 = min(timed(lambda: torch.bmm(x, w13, out=o1)),
+                 timed(lambda: torch.bmm(x, w13t.transpose(1, 2), out=o1)))
+        g2 = min(timed(lambda: torch.bmm(hh, w2, out=o2)),
+                 timed(lambda: torch.bmm(hh, w2t.transpose(1, 2), out=o2)))
+        res[name] = {"experts": E, "rows_per_expert": R, "gemm1_us": g1, "gemm2_us": g2}
+        del x, hh, w13, w2, w13t, w2t, o1, o2
+        torch.cuda.empty_cache()
+    total = sum(v["gemm1_us"] + v["gemm2_us"] for v in res.values())
+    flop = 32768 * 6 * H * I
+    return {"library": "hipBLASLt via torch.bmm", "pools": res, "total_us": total,
+            "tflops": flop / (total * 1e-6) / 1e12}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -293,6 +338,9 @@ def main():
         return
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
+        return
+    if args.vendor_gemm:
+        print(json.dumps(vendor_gemm_bench(dev)), flush=True)
         return
     if args.fingerprint_only:
         print(json.dumps(fingerprint_bench(args, dev)), flush=True)

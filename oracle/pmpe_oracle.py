@@ -1,4 +1,5 @@
-"""CPU oracle of the policy-masked MoE layer forward.
+"""CPU oracle of the policy-masked MoE layer: forward, private-only backward, and the
+weight fingerprint.
 
 TEST INFRASTRUCTURE ONLY. Only the tests, the package smoke check and the
 benchmark's CPU-baseline leg may import this module. It shares no code with the
@@ -26,6 +27,11 @@ computes, following Policy-Masked Private Experts (arXiv 2608.06690):
              mask; kept only to show what the mask prevents
 * audit      per-request private rows, deny violations (App. B.2 "route counters
              indexed by row and layer"; App. F.1)
+* backward   gradients of the layer for an upstream gradient with only the private
+             experts and private router rows trainable (G2 of Sec. 2.2; Sec. 3.2:
+             only the private gate and experts require gradients); the input gradient
+             flows through frozen public and shared experts and the router
+* fingerprint  SHA-256 tree over the bytes of frozen weights (Sec. 3.2; App. C.1)
 
 Readings where the paper is silent (the paper gives only the mask and top-k):
 
@@ -42,6 +48,12 @@ Readings where the paper is silent (the paper gives only the mask and top-k):
   never counted by the audit.
 * Expert math is exact fp64 on the (fp32 or bf16) input values with no
   intermediate rounding.
+
+Backward readings: the selection is the forward's (piecewise constant), gradients flow
+through the gate values; the softmax derivative uses the fp64 softmax of the fp32
+logits. It is pinned to torch autograd of a separately written fp64 forward, to central
+finite differences and to exact special cases (all deny: no private gradient; k = 1
+RENORM: no router gradient).
 
 Parity of the floating-point expert outputs is pinned only by special cases (a
 one-expert pool reduces to a dense SwiGLU MLP; all-deny equals a plain public-only
@@ -338,6 +350,128 @@ def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_pri
             acc += ysh[i]
         out[i] = acc
     return LayerResult(rt, dp, out, toks, hook, dp.count)
+
+
+# ----------------------------------------------------------------------------
+# Private-only backward (G2 of Sec. 2.2; Sec. 3.2 training and checkpointing)
+# ----------------------------------------------------------------------------
+
+def swiglu_backward(X: np.ndarray, w13: np.ndarray, w2: np.ndarray, dY: np.ndarray):
+    """Gradients of one SwiGLU expert Y = (silu(X Wg^T) * (X Wu^T)) Wd^T for the upstream
+    gradient dY: returns (dX, dW13, dW2) with dW13 = [dWg; dWu] of shape [2I, H] and
+    dW2 = dWd of shape [H, I]. silu'(g) = s (1 + g (1 - s)) with s = sigmoid(g)."""
+    X = np.asarray(X, np.float64)
+    w13 = np.asarray(w13, np.float64)
+    w2 = np.asarray(w2, np.float64)
+    dY = np.asarray(dY, np.float64)
+    I = w13.shape[0] // 2
+    Wg, Wu = w13[:I], w13[I:]
+    G = X @ Wg.T
+    U = X @ Wu.T
+    S = 1.0 / (1.0 + np.exp(-G))
+    A = G * S * U                       # h = silu(G) * U
+    dA = dY @ w2                        # [n, I]
+    dW2 = dY.T @ A                      # [H, I]
+    dG = dA * U * S * (1.0 + G * (1.0 - S))
+    dU = dA * G * S
+    dX = dG @ Wg + dU @ Wu
+    dW13 = np.concatenate([dG.T @ X, dU.T @ X], axis=0)
+    return dX, dW13, dW2
+
+
+def gate_backward(z_sel: np.ndarray, z_pool: np.ndarray, sel_pos: np.ndarray, dg: np.ndarray,
+                  mode: str) -> np.ndarray:
+    """Logit gradient over the token's pool from the gate gradient dg of its k selected
+    experts (positions sel_pos in the pool). Exact fp64 softmax derivative:
+    RENORM   g = softmax(z_sel):  dz_j = g_j (dg_j - sum_i g_i dg_i) on the selection;
+    POOL     p = softmax(z_pool), g_j = p_j:  dz_e = p_e ([e selected] dg_e - sum_i p_i dg_i)."""
+    dz = np.zeros(len(z_pool), np.float64)
+    dg = np.asarray(dg, np.float64)
+    if mode == GATE_RENORM:
+        zs = np.asarray(z_sel, np.float64)
+        g = np.exp(zs - zs.max())
+        g /= g.sum()
+        dz[sel_pos] = g * (dg - (g * dg).sum())
+    elif mode == GATE_POOL_SOFTMAX:
+        zp = np.asarray(z_pool, np.float64)
+        p = np.exp(zp - zp.max())
+        p /= p.sum()
+        up = np.zeros(len(zp), np.float64)
+        up[sel_pos] = dg
+        dz = p * (up - (p[sel_pos] * dg).sum())
+    else:
+        raise ValueError(mode)
+    return dz
+
+
+@dataclass
+class LayerGrads:
+    route: Route
+    dx: np.ndarray          # [T, H] input gradient (through every expert, router, shared)
+    dw13_priv: np.ndarray   # [n_priv, 2I, H]
+    dw2_priv: np.ndarray    # [n_priv, H, I]
+    dwr_priv: np.ndarray    # [n_priv, H] private router rows (the private gate)
+    grad_rows: np.ndarray   # [n_priv] rows that entered each private expert's gradient
+
+
+def layer_backward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_priv, w2_priv,
+                   words: Sequence[int], k: int, dout: np.ndarray, gate_mode: str = GATE_RENORM,
+                   w13_sh=None, w2_sh=None, soft: bool = False) -> LayerGrads:
+    """Backward of layer_forward for the upstream gradient dout [T, H], with only the
+    private experts and the private router rows trainable: public experts, public
+    router rows, the logit bias and shared experts are frozen, so no gradient of theirs
+    is formed, but the input gradient flows through all of them. The route (a
+    piecewise-constant selection) is the forward's; gradients flow through the gate
+    values of the selected experts."""
+    x = np.asarray(x)
+    T, H = x.shape
+    n_pub = wr_pub.shape[0]
+    n_priv = wr_priv.shape[0] if wr_priv is not None else 0
+    E = n_pub + n_priv
+    dout = np.asarray(dout, np.float64)
+    rt = route(x, wr_pub, wr_priv, bias, words, k, gate_mode, soft=soft)
+    x64 = np.asarray(x, np.float64)
+    dx = np.zeros((T, H), np.float64)
+    I = (np.asarray(w13_priv[0]).shape[0] // 2) if n_priv else np.asarray(w13_pub[0]).shape[0] // 2
+    dw13 = np.zeros((n_priv, 2 * I, H), np.float64)
+    dw2 = np.zeros((n_priv, H, I), np.float64)
+    dwr = np.zeros((n_priv, H), np.float64)
+    grad_rows = np.zeros(n_priv, np.int64)
+    dg = np.zeros((T, k), np.float64)
+    for e in range(E):
+        hit = rt.idx == e
+        rows = np.nonzero(hit.any(axis=1))[0]
+        if len(rows) == 0:
+            continue
+        slot = np.argmax(hit[rows], axis=1)
+        w13 = w13_pub[e] if e < n_pub else w13_priv[e - n_pub]
+        w2 = w2_pub[e] if e < n_pub else w2_priv[e - n_pub]
+        X = x64[rows]
+        Y = swiglu(X, w13, w2)
+        g = rt.gate[rows, slot].astype(np.float64)
+        dg[rows, slot] = (dout[rows] * Y).sum(axis=1)
+        dX, dW13, dW2 = swiglu_backward(X, w13, w2, g[:, None] * dout[rows])
+        dx[rows] += dX
+        if e >= n_pub:
+            dw13[e - n_pub] = dW13
+            dw2[e - n_pub] = dW2
+            grad_rows[e - n_pub] = len(rows)
+    taus = rt.allow.astype(np.int64)
+    wr_all = np.concatenate([np.asarray(wr_pub, np.float64)]
+                            + ([np.asarray(wr_priv, np.float64)] if n_priv else []), axis=0)
+    for t in range(T):
+        ids = np.arange(E) if soft else pool(int(taus[t]), n_pub, n_priv)
+        sel_pos = np.searchsorted(ids, rt.idx[t])
+        z_pool = rt.z[t]
+        dz = gate_backward(z_pool[sel_pos], z_pool, sel_pos, dg[t], gate_mode)
+        dx[t] += dz @ wr_all[ids]
+        priv = ids >= n_pub
+        if priv.any():
+            dwr[ids[priv] - n_pub] += dz[priv][:, None] * x64[t][None, :]
+    if w13_sh is not None:
+        dxs, _, _ = swiglu_backward(x64, w13_sh, w2_sh, dout)
+        dx += dxs
+    return LayerGrads(rt, dx, dw13, dw2, dwr, grad_rows)
 
 
 # ----------------------------------------------------------------------------

@@ -527,3 +527,138 @@ def test_fingerprint_set_of_small_buffers_is_hash_of_hashes():
     parts = [b"abc", b"", bytes(range(200))]
     assert O.fingerprint_set(parts) == h(h(b"abc") + h(b"") + h(bytes(range(200))))
     assert O.fingerprint_set(parts) != O.fingerprint_set(parts[::-1])
+
+
+# ----------------------------------------------------------------------------
+# Private-only backward: pinned to torch autograd of an independently written fp64
+# forward, to central finite differences, and to exact special cases
+# ----------------------------------------------------------------------------
+
+def _textbook_layer_torch(x, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_priv, w2_priv, taus, k,
+                          mode, w13_sh=None, w2_sh=None, soft=False):
+    """Differentiable fp64 forward written from the definitions: per token, the permitted
+    pool (private if tau else public; everything when soft), logits x.W_r + b, top-k,
+    gates, gated sum of SwiGLU experts, plus the shared SwiGLU."""
+    import torch
+    n_pub, n_priv = wr_pub.shape[0], wr_priv.shape[0]
+    wr = torch.cat([wr_pub, wr_priv], 0)
+    w13 = torch.cat([w13_pub, w13_priv], 0)
+    w2 = torch.cat([w2_pub, w2_priv], 0)
+    I = w13.shape[1] // 2
+
+    def mlp(v, a, b):
+        ii = a.shape[0] // 2
+        return (torch.nn.functional.silu(a[:ii] @ v) * (a[ii:] @ v)) @ b.T
+
+    rows, sels = [], []
+    for t in range(x.shape[0]):
+        if soft:
+            ids = torch.arange(n_pub + n_priv)
+        elif taus[t]:
+            ids = torch.arange(n_pub, n_pub + n_priv)
+        else:
+            ids = torch.arange(n_pub)
+        z = wr[ids] @ x[t] + (bias[ids] if bias is not None else 0.0)
+        vals, pos = torch.topk(z, k)
+        g = torch.softmax(vals, 0) if mode == "renorm" else torch.softmax(z, 0)[pos]
+        acc = sum(g[j] * mlp(x[t], w13[ids[pos[j]]], w2[ids[pos[j]]]) for j in range(k))
+        if w13_sh is not None:
+            acc = acc + mlp(x[t], w13_sh, w2_sh)
+        rows.append(acc)
+        sels.append(sorted(int(i) for i in ids[pos]))
+    del I
+    return torch.stack(rows), sels
+
+
+def _bwd_case(seed, mode="renorm", soft=False, shared=False, taus=None, T=12, H=16, I=8,
+              n_pub=6, n_priv=4, k=2):
+    rng = np.random.default_rng(seed)
+    f = lambda *s: rng.standard_normal(s) * 0.5  # noqa: E731
+    c = dict(x=f(T, H), wr_pub=f(n_pub, H), wr_priv=f(n_priv, H), bias=f(n_pub + n_priv) * 0.1,
+             w13_pub=f(n_pub, 2 * I, H), w2_pub=f(n_pub, H, I), w13_priv=f(n_priv, 2 * I, H),
+             w2_priv=f(n_priv, H, I), dout=f(T, H))
+    if shared:
+        c["w13_sh"], c["w2_sh"] = f(2 * 6, H), f(H, 6)
+    else:
+        c["w13_sh"] = c["w2_sh"] = None
+    if taus is None:
+        taus = rng.integers(0, 2, T)
+    words = [O.ALLOW_WORD if t else O.DENY_WORD for t in taus]
+    return c, np.asarray(taus), words, mode, soft, k
+
+
+def _oracle_grads(c, words, mode, soft, k):
+    return O.layer_backward(c["x"], c["wr_pub"], c["wr_priv"], c["bias"], c["w13_pub"], c["w2_pub"],
+                            c["w13_priv"], c["w2_priv"], words, k, c["dout"], mode,
+                            c["w13_sh"], c["w2_sh"], soft=soft)
+
+
+@pytest.mark.parametrize("mode,soft,shared", [("renorm", False, False), ("pool_softmax", False, False),
+                                              ("renorm", True, False), ("renorm", False, True),
+                                              ("pool_softmax", True, True)])
+def test_backward_equals_autograd_of_textbook_forward(mode, soft, shared):
+    import torch
+    c, taus, words, mode, soft, k = _bwd_case(11, mode, soft, shared)
+    g = _oracle_grads(c, words, mode, soft, k)
+    tt = {n: (None if v is None else torch.tensor(v, dtype=torch.float64, requires_grad=True))
+          for n, v in c.items()}
+    out, sels = _textbook_layer_torch(tt["x"], tt["wr_pub"], tt["wr_priv"], tt["bias"], tt["w13_pub"],
+                                      tt["w2_pub"], tt["w13_priv"], tt["w2_priv"], taus, k, mode,
+                                      tt["w13_sh"], tt["w2_sh"], soft)
+    assert all(list(g.route.idx[t]) == sels[t] for t in range(len(sels)))
+    (out * tt["dout"]).sum().backward()
+    rel = lambda a, b: np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)  # noqa: E731
+    assert rel(g.dx, tt["x"].grad.numpy()) < 1e-6
+    assert rel(g.dw13_priv, tt["w13_priv"].grad.numpy()) < 1e-6
+    assert rel(g.dw2_priv, tt["w2_priv"].grad.numpy()) < 1e-6
+    assert rel(g.dwr_priv, tt["wr_priv"].grad.numpy()) < 1e-6
+    # every private expert that some token selected received rows and a nonzero gradient
+    used = np.unique(g.route.idx[g.route.idx >= 6]) - 6
+    assert np.all(g.grad_rows[used] > 0)
+    assert np.all(np.abs(g.dw13_priv[used]).sum(axis=(1, 2)) > 0)
+
+
+def test_backward_central_differences():
+    """A few entries of each gradient against (L(p + e) - L(p - e)) / 2e of the fp64
+    textbook forward, L = sum(dout * out)."""
+    import torch
+    c, taus, words, mode, soft, k = _bwd_case(12, "renorm", False, False)
+    g = _oracle_grads(c, words, mode, soft, k)
+
+    def loss():
+        tt = {n: (None if v is None else torch.tensor(v, dtype=torch.float64)) for n, v in c.items()}
+        out, _ = _textbook_layer_torch(tt["x"], tt["wr_pub"], tt["wr_priv"], tt["bias"], tt["w13_pub"],
+                                       tt["w2_pub"], tt["w13_priv"], tt["w2_priv"], taus, k, mode)
+        return float((out * tt["dout"]).sum())
+
+    eps = 1e-6
+    for name, idx, ref in [("x", (3, 5), g.dx[3, 5]), ("w13_priv", (1, 2, 7), g.dw13_priv[1, 2, 7]),
+                           ("w13_priv", (2, 9, 0), g.dw13_priv[2, 9, 0]),
+                           ("w2_priv", (0, 4, 3), g.dw2_priv[0, 4, 3]),
+                           ("wr_priv", (3, 11), g.dwr_priv[3, 11]), ("x", (0, 0), g.dx[0, 0])]:
+        v = c[name][idx]
+        c[name][idx] = v + eps
+        lp = loss()
+        c[name][idx] = v - eps
+        lm = loss()
+        c[name][idx] = v
+        assert abs((lp - lm) / (2 * eps) - ref) <= 1e-6 * max(1.0, abs(ref)), (name, idx)
+
+
+def test_backward_all_deny_forms_no_private_gradient():
+    c, taus, words, mode, soft, k = _bwd_case(13, taus=np.zeros(12, np.int64))
+    g = _oracle_grads(c, words, mode, soft, k)
+    assert not g.dw13_priv.any() and not g.dw2_priv.any() and not g.dwr_priv.any()
+    assert not g.grad_rows.any() and np.abs(g.dx).sum() > 0
+
+
+def test_backward_k1_renorm_gate_is_constant():
+    """With k = 1 and RENORM the gate is identically 1, so the router gets no gradient
+    and the input gradient is the selected expert's alone."""
+    c, taus, words, mode, soft, k = _bwd_case(14, k=1, taus=np.ones(12, np.int64))
+    g = _oracle_grads(c, words, mode, soft, k)
+    assert not g.dwr_priv.any()
+    t = 4
+    e = int(g.route.idx[t, 0]) - 6
+    dX, _, _ = O.swiglu_backward(c["x"][t:t + 1], c["w13_priv"][e], c["w2_priv"][e], c["dout"][t:t + 1])
+    assert np.allclose(g.dx[t], dX[0], rtol=1e-12, atol=1e-12)
