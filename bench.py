@@ -62,6 +62,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true")
     p.add_argument("--no-fingerprint", action="store_true")
+    p.add_argument("--no-backward", action="store_true")
+    p.add_argument("--backward-only", action="store_true",
+                   help="only time the private-only backward of the Qwen-shaped layer")
     p.add_argument("--vendor-gemm", action="store_true",
                    help="only time hipBLASLt on the same expert GEMM shapes (context)")
     p.add_argument("--fingerprint-only", action="store_true",
@@ -268,6 +271,51 @@ def fingerprint_bench(args, dev):
             "peak_gbs": peak_gbs, "frac": gbs / peak_gbs, "reps": reps}
 
 
+def backward_bench(args, dev):
+    """Private-only backward of the Qwen-shaped layer (4 allow + 4 deny requests) after
+    its forward: per-call time and the MFMA rate of its GEMM work."""
+    import torch
+    import workloads as W
+    cfg, layer, x, words, req_off, audit, bufs, req = setup("qwen", dev)
+    # training forward: keeps the gate and up projections for the backward
+    layer.forward(x, words, audit, req_off, train=True)
+    dout = W.make_dout(cfg, device=dev)
+    g = layer.grad_buffers(cfg.tokens)
+    for _ in range(max(1, args.warmup // 2)):
+        layer.backward(x, dout, bufs, g)
+    torch.cuda.synchronize()
+    reps = max(5, args.steps // 2)
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        layer.backward(x, dout, bufs, g)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    us = sum(times) / len(times)
+    counts = bufs.expert_count.cpu()
+    R = cfg.tokens * cfg.top_k
+    Rp = int(counts[cfg.n_pub:].sum())
+    H, I = cfg.hidden, cfg.inter
+    # algorithmic: dh (2 R H I) and row input gradients (4 R I H) over every row, weight
+    # gradients (6 Rp H I) over the private rows (the gate and up projections come from
+    # the training forward)
+    alg = 6 * H * I * (R + Rp)
+    executed = alg
+    res = {"workload": "qwen3-30b-a3b-shaped layer backward, private experts and private "
+                       "router rows trainable, 4 allow + 4 deny requests",
+           "us_per_call": us, "us_p10": sorted(times)[len(times) // 10],
+           "us_p90": sorted(times)[min(len(times) - 1, 9 * len(times) // 10)],
+           "rows": R, "private_rows": Rp, "flop_algorithmic": alg, "flop_executed": executed,
+           "tflops_algorithmic": alg / (us * 1e-6) / 1e12,
+           "tflops_executed": executed / (us * 1e-6) / 1e12,
+           "frac_algorithmic": alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, "reps": reps}
+    del layer, x, bufs, g, dout
+    torch.cuda.empty_cache()
+    return res
+
+
 def vendor_gemm_bench(dev, reps=20):
     """Context only: hipBLASLt (torch.bmm) on the Qwen layer's per-expert GEMM shapes with
     uniform rows (128 per public expert, 512 per private expert), without the SwiGLU, the
@@ -339,6 +387,9 @@ def main():
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
         return
+    if args.backward_only:
+        print(json.dumps(backward_bench(args, dev)), flush=True)
+        return
     if args.vendor_gemm:
         print(json.dumps(vendor_gemm_bench(dev)), flush=True)
         return
@@ -393,6 +444,8 @@ def main():
 
     if not args.no_decode:
         out["decode"] = decode_bench(args, dev)
+    if not args.no_backward:
+        out["backward"] = backward_bench(args, dev)
     if not args.no_fingerprint:
         out["fingerprint"] = fingerprint_bench(args, dev)
 

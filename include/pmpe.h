@@ -222,6 +222,24 @@ pmpe_status pmpe_expert_ffn(const pmpe_layer_desc* d, int32_t T, const void* x_p
                             size_t ws_bytes, pmpe_stream_t stream);
 
 /*
+ * pmpe_expert_ffn_train - pmpe_expert_ffn that also stores, for every routed row r, the
+ * fp32 gate and up projections ab[r] = [W1 x; W3 x] (2I values) that pmpe_backward needs
+ * (Sec. 3.2: the private pool is trained through the same forward). Same arguments and
+ * errors as pmpe_expert_ffn plus ab (device, [T*k, 2I] fp32, 16-byte aligned, not NULL);
+ * bf16 only (PMPE_ERR_DTYPE otherwise). The shared group's projections are not stored.
+ * Rows of private experts whose weights are NULL are not executed and their ab rows are
+ * left unwritten.
+ */
+pmpe_status pmpe_expert_ffn_train(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                                  const void* x, const int32_t* expert_count,
+                                  const int32_t* expert_offset, const int32_t* row_token,
+                                  const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                                  const void* w2_priv, const void* w13_sh, const void* w2_sh,
+                                  void* y_shared, void* y_perm, uint32_t* audit_token_rows,
+                                  uint32_t* audit_priv_calls, uint32_t* dev_status, float* ab,
+                                  void* ws, size_t ws_bytes, pmpe_stream_t stream);
+
+/*
  * pmpe_combine - merge the selected experts' outputs into the layer output.
  * (Merge into the frozen upper transformer, Fig. 1 and Sec. 3.1.)
  *
@@ -254,6 +272,63 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
                        const uint8_t* allow, const int32_t* req_offset, int32_t R,
                        uint64_t* req_private_rows, uint64_t* total_private_rows,
                        uint32_t* deny_violations, pmpe_stream_t stream);
+
+/*
+ * pmpe_backward - private-only backward of one layer for an upstream gradient dout.
+ * (G2 of Sec. 2.2: frozen public parameters are not optimised and stay unchanged;
+ * Sec. 3.2: only the private gate and the private expert weights require gradients.)
+ *
+ * Gradients are formed for the private expert weights and the private router rows
+ * only; the public experts, the public router rows and the logit bias are frozen and
+ * no gradient of theirs is ever formed or written. The input gradient flows through
+ * every expert the forward executed (public ones included) and through the router:
+ *
+ *   dg_tj   = dout_t . y_{e_tj}(x_t)                     (y_perm of the forward)
+ *   dz_tj   = g_tj (dg_tj - sum_i g_ti dg_ti)            (RENORM gates)
+ *   dx_t    = sum_j [ W13_e^T (da; db)_tj + dz_tj W_r[e_tj] ]
+ *   dW2_p   = sum over rows of private expert p of (g dout_t) h^T
+ *   dW13_p  = sum over rows of p of (da; db) x_t^T
+ *   dW_r[p] = sum over rows of p of dz x_t
+ * with a = W1 x, b = W3 x, s = sigmoid(a), h = a s b, dh = W2^T (g dout_t),
+ * da = dh b s (1 + a (1 - s)), db = dh a s. The route (selection and gates) is the
+ * forward's. Every output element is summed by one thread in a fixed order: two calls
+ * on the same inputs give bitwise equal results.
+ *
+ * Supported: bf16, PMPE_GATE_RENORM_TOPK, n_shared == 0, inter a multiple of 128;
+ * either route mode (under PMPE_ROUTE_SOFT, deny rows that reached private experts
+ * also feed private gradients - the control shows what the mask prevents).
+ *
+ *   x [T, H], dout [T, H]                       bf16
+ *   topk_idx, topk_gate [T*k], expert_count, expert_offset [E], row_token, token_row
+ *   [T*k], y_perm [T*k, H]                      the forward's route, dispatch and
+ *                                               expert outputs
+ *   wr_pub, wr_priv, w13_*, w2_*                the forward's weights
+ *   ab [T*k, 2I] fp32 or NULL                   the gate and up projections saved by
+ *                                               pmpe_expert_ffn_train; NULL recomputes
+ *                                               them (one more grouped GEMM)
+ *   dx [T, H] fp32                              out
+ *   dw13_priv [n_priv, 2I, H], dw2_priv [n_priv, H, I], dwr_priv [n_priv, H]
+ *                                               fp32 out, overwritten (an expert with
+ *                                               no rows gets zeros)
+ *   grad_rows [n_priv] uint32 out or NULL       rows that entered each private
+ *                                               expert's gradient
+ *   ws                                          pmpe_backward_workspace_bytes(d, T)
+ *                                               bytes, 16-byte aligned
+ *
+ * Errors: PMPE_ERR_DTYPE (not bf16), PMPE_ERR_SHAPE (unsupported gate mode, shared
+ * experts or inter), PMPE_ERR_NULL, PMPE_ERR_ALIGN, PMPE_ERR_WORKSPACE.
+ */
+size_t pmpe_backward_workspace_bytes(const pmpe_layer_desc* d, int32_t T);
+
+pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, const void* dout,
+                          const int32_t* topk_idx, const float* topk_gate,
+                          const int32_t* expert_count, const int32_t* expert_offset,
+                          const int32_t* row_token, const int32_t* token_row, const void* y_perm,
+                          const float* wr_pub, const float* wr_priv, const void* w13_pub,
+                          const void* w2_pub, const void* w13_priv, const void* w2_priv,
+                          const float* ab, float* dx, float* dw13_priv, float* dw2_priv,
+                          float* dwr_priv, uint32_t* grad_rows, void* ws, size_t ws_bytes,
+                          pmpe_stream_t stream);
 
 /*
  * pmpe_fingerprint - SHA-256 tree digest of a device buffer, to show that the frozen

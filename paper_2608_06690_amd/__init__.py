@@ -6,8 +6,9 @@ from ._native import (PMPE_BF16, PMPE_F32, PMPE_GATE_POOL_SOFTMAX, PMPE_GATE_REN
                       PMPE_POLICY_ALLOW, PMPE_POLICY_DENY, PMPE_ROUTE_MASKED, PMPE_ROUTE_SOFT,
                       PMPE_FP_FANOUT, PMPE_FP_LEAF_BYTES, LayerDesc, PmpeError,
                       fingerprint_tensors, make_desc, pmpe_fingerprint,
-                      pmpe_fingerprint_workspace_bytes,
+                      pmpe_fingerprint_workspace_bytes, pmpe_backward,
+                      pmpe_backward_workspace_bytes, pmpe_expert_ffn_train,
                       pmpe_audit, pmpe_check_desc, pmpe_combine, pmpe_dispatch, pmpe_expert_ffn,
                       pmpe_route, pmpe_version, pmpe_workspace_bytes)
-from .layer import AuditBuffers, LayerBuffers, PolicyMaskedMoE  # noqa: F401
+from .layer import AuditBuffers, GradBuffers, LayerBuffers, PolicyMaskedMoE  # noqa: F401
 from .policy import policy_word, request_offsets, resolve_policy, token_policy_words  # noqa: F401

@@ -79,6 +79,12 @@ _lib.pmpe_combine.argtypes = [_DESC, _I32] + [_P] * 5 + [_P]
 _lib.pmpe_audit.restype = _I32
 _lib.pmpe_audit.argtypes = [_DESC, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]
 
+_lib.pmpe_backward_workspace_bytes.restype = _SZ
+_lib.pmpe_backward_workspace_bytes.argtypes = [_DESC, _I32]
+_lib.pmpe_backward.restype = _I32
+_lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 21 + [_P, _SZ, _P]
+_lib.pmpe_expert_ffn_train.restype = _I32
+_lib.pmpe_expert_ffn_train.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
 _lib.pmpe_fingerprint_workspace_bytes.restype = _SZ
 _lib.pmpe_fingerprint_workspace_bytes.argtypes = [ctypes.c_uint64]
 _lib.pmpe_fingerprint.restype = _I32
@@ -86,7 +92,8 @@ _lib.pmpe_fingerprint.argtypes = [_P, ctypes.c_uint64, _P, _P, _SZ, _P]
 
 EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_check_desc",
             "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
-            "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint"]
+            "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint", "pmpe_backward_workspace_bytes",
+            "pmpe_backward", "pmpe_expert_ffn_train"]
 
 PMPE_FP_LEAF_BYTES = 1024
 PMPE_FP_FANOUT = 16
@@ -173,6 +180,33 @@ def pmpe_audit(desc, T, audit_token_rows, allow, req_offset, R, req_private_rows
     _check(_lib.pmpe_audit(ctypes.byref(desc), T, _ptr(audit_token_rows), _ptr(allow),
                            _ptr(req_offset), R, _ptr(req_private_rows), _ptr(total_private_rows),
                            _ptr(deny_violations), _stream(stream)), "pmpe_audit")
+
+
+def pmpe_backward_workspace_bytes(desc: LayerDesc, T: int) -> int:
+    return int(_lib.pmpe_backward_workspace_bytes(ctypes.byref(desc), T))
+
+
+def pmpe_expert_ffn_train(desc, T, x_perm, x, expert_count, expert_offset, row_token, w13_pub,
+                          w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm,
+                          audit_token_rows, audit_priv_calls, dev_status, ab, ws,
+                          stream=None) -> None:
+    _check(_lib.pmpe_expert_ffn_train(
+        ctypes.byref(desc), T, _ptr(x_perm), _ptr(x), _ptr(expert_count), _ptr(expert_offset),
+        _ptr(row_token), _ptr(w13_pub), _ptr(w2_pub), _ptr(w13_priv), _ptr(w2_priv), _ptr(w13_sh),
+        _ptr(w2_sh), _ptr(y_shared), _ptr(y_perm), _ptr(audit_token_rows), _ptr(audit_priv_calls),
+        _ptr(dev_status), _ptr(ab), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)), "pmpe_expert_ffn_train")
+
+
+def pmpe_backward(desc, T, x, dout, topk_idx, topk_gate, expert_count, expert_offset, row_token,
+                  token_row, y_perm, wr_pub, wr_priv, w13_pub, w2_pub, w13_priv, w2_priv, ab, dx,
+                  dw13_priv, dw2_priv, dwr_priv, grad_rows, ws, stream=None) -> None:
+    _check(_lib.pmpe_backward(
+        ctypes.byref(desc), T, _ptr(x), _ptr(dout), _ptr(topk_idx), _ptr(topk_gate),
+        _ptr(expert_count), _ptr(expert_offset), _ptr(row_token), _ptr(token_row), _ptr(y_perm),
+        _ptr(wr_pub), _ptr(wr_priv), _ptr(w13_pub), _ptr(w2_pub), _ptr(w13_priv), _ptr(w2_priv),
+        _ptr(ab), _ptr(dx), _ptr(dw13_priv), _ptr(dw2_priv), _ptr(dwr_priv), _ptr(grad_rows), _ptr(ws),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)), "pmpe_backward")
 
 
 def pmpe_fingerprint_workspace_bytes(nbytes: int) -> int:

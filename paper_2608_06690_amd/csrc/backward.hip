@@ -1,0 +1,481 @@
+// Private-only backward of one policy-masked MoE layer.
+//
+// Only the private experts and the private router rows are trainable (G2 of Sec. 2.2:
+// frozen public parameters are not optimised; Sec. 3.2: only the private gate and
+// expert weights require gradients). The input gradient still flows through every
+// executed expert (public ones too), through the router logits of the selected
+// experts and the gates. The route is the forward's: the selection is piecewise
+// constant, so gradients flow through the gate values only.
+//
+// For a row r = (token t, selected expert e, gate g) with upstream gradient G_t:
+//   dg      = G_t . y_e(x_t)                      (forward expert output, y_perm)
+//   u_r     = g G_t                               (bf16, the expert's upstream row)
+//   [a; b]  = W13_e x_t                           (fp32, saved by the forward or recomputed)
+//   dh      = W2_e^T u_r
+//   da      = dh b s (1 + a (1 - s)),  db = dh a s,  s = sigmoid(a),  h = a s b
+//   dx_t   += W13_e^T [da; db]
+//   dW2_e  += u_r h^T,  dW13_e += [da; db] x_t^T   (private e only)
+// and per token, with the k selected gates renormalised by a softmax (RENORM):
+//   dz_j = g_j (dg_j - sum_i g_i dg_i),  dx_t += sum_j dz_j W_r[e_j],
+//   dW_r[e] += dz x_t for private e.
+//
+// Kernels: a per-token row pass (dg, dz, u rows, gathered x rows); launches of one
+// grouped bf16 MFMA GEMM template: the gate and up projections (only when the forward
+// did not save them), dh with the SwiGLU backward in its epilogue, the row input
+// gradients, and the weight gradients, which cover the private experts only, so no
+// public gradient is ever formed; then per-token input-gradient and
+// per-private-expert router-gradient reductions. Every output element is summed by
+// one thread in a fixed order, so the results are bitwise reproducible.
+#include "pmpe_internal.h"
+
+namespace pmpe {
+namespace {
+
+constexpr int BT = 256;      // threads of every kernel here
+constexpr int TM = 128;      // GEMM tile rows (M)
+constexpr int TN = 128;      // GEMM tile columns (N)
+constexpr int TK = 64;       // GEMM K step
+constexpr int ROWB = 2 * TK; // bytes of one LDS operand row (64 bf16)
+constexpr int OPB = TM * ROWB;  // bytes of one LDS operand tile (16 KiB)
+constexpr int MAXG = 2 * PMPE_MAX_POOL;
+
+// ---------------------------------------------------------------------------
+// Per-token row pass
+// ---------------------------------------------------------------------------
+// Block t: dg_j = G_t . y_perm[r_j] (fixed-order block reduction), dz_j (RENORM),
+// dY[r_j] = bf16(g_j G_t), Xp[r_j] = x_t, dz_row[r_j] = dz_j.
+__global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
+  __shared__ float s_part[BT / 64][PMPE_MAX_TOPK];
+  __shared__ float s_dz[PMPE_MAX_TOPK];
+  __shared__ int s_row[PMPE_MAX_TOPK];
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int H = a.H, k = a.k, nch = H / 8;
+  const uint16_t* G = (const uint16_t*)a.dout + (size_t)t * H;
+  const uint16_t* y = (const uint16_t*)a.y_perm;
+  if (tid < k) s_row[tid] = a.token_row[t * k + tid];
+  __syncthreads();
+  float part[PMPE_MAX_TOPK];
+#pragma unroll
+  for (int j = 0; j < PMPE_MAX_TOPK; ++j) part[j] = 0.f;
+  for (int c = tid; c < nch; c += BT) {
+    const u32x4 gv = *(const u32x4*)(G + c * 8);
+    float gf[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      gf[2 * q] = bf16_to_f32(gv[q] & 0xFFFFu);
+      gf[2 * q + 1] = bf16_to_f32(gv[q] >> 16);
+    }
+#pragma unroll
+    for (int j = 0; j < PMPE_MAX_TOPK; ++j) {
+      if (j < k) {
+        const u32x4 yv = *(const u32x4*)(y + (size_t)s_row[j] * H + c * 8);
+        float s = 0.f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          s += gf[2 * q] * bf16_to_f32(yv[q] & 0xFFFFu) + gf[2 * q + 1] * bf16_to_f32(yv[q] >> 16);
+        part[j] += s;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < PMPE_MAX_TOPK; ++j) {
+    if (j < k) {
+      const float v = wave_sum(part[j]);
+      if (lane == 0) s_part[wave][j] = v;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float dg[PMPE_MAX_TOPK], g[PMPE_MAX_TOPK], sum = 0.f;
+    for (int j = 0; j < k; ++j) {
+      float v = 0.f;
+      for (int w = 0; w < BT / 64; ++w) v += s_part[w][j];
+      dg[j] = v;
+      g[j] = a.topk_gate[t * k + j];
+      sum += g[j] * v;
+    }
+    for (int j = 0; j < k; ++j) s_dz[j] = g[j] * (dg[j] - sum);
+  }
+  __syncthreads();
+  if (tid < k) a.dz_row[s_row[tid]] = s_dz[tid];
+  const uint16_t* xt = (const uint16_t*)a.x + (size_t)t * H;
+  for (int c = tid; c < nch; c += BT) {
+    const u32x4 gv = *(const u32x4*)(G + c * 8);
+    const u32x4 xv = *(const u32x4*)(xt + c * 8);
+    for (int j = 0; j < k; ++j) {
+      const float g = a.topk_gate[t * k + j];
+      u32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        o[q] = pack_bf16x2(g * bf16_to_f32(gv[q] & 0xFFFFu), g * bf16_to_f32(gv[q] >> 16));
+      const size_t r = (size_t)s_row[j];
+      *(u32x4*)(a.dY + r * H + c * 8) = o;
+      *(u32x4*)(a.Xp + r * H + c * 8) = xv;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Grouped bf16 GEMM, C[M, N] = A[M, K] B[N, K]^T per group, fp32 accumulation
+// ---------------------------------------------------------------------------
+// Operand views: a non-transposed operand is stored with K contiguous (row m at
+// P + row * ld); a transposed one is stored [K, M] with M contiguous (element (m, k) at
+// P + k * ld + m). Both are staged through registers into the same K-contiguous LDS
+// layout; a transposed operand is turned in registers from 4 K-rows x 8 columns into
+// 8 rows x 4 K values per thread.
+//
+// ROWS mode: group g owns rows [offset[g], offset[g] + count[g]) of A and of C, K and N
+// are fixed, B is the group's weight matrix. K-ROWS mode: the contraction runs over the
+// group's rows (K = count[g]; rows past it are read as zeros), M and N are fixed, and
+// C is the group's own [M, N] matrix.
+enum { EPI_F32 = 0, EPI_SWIGLU_BWD = 1 };
+
+struct GemmArgs {
+  const uint16_t* A;
+  int lda;
+  const uint16_t* B;       // K-ROWS: activation rows; ROWS: public weight base
+  const uint16_t* B_priv;  // ROWS: private weight base
+  size_t strideB;          // ROWS: elements per expert weight matrix
+  int ldb;
+  float* C;
+  int ldc;
+  size_t strideC;          // K-ROWS: elements per group output
+  const int32_t* count;
+  const int32_t* offset;
+  int g_begin, g_end, n_pub;
+  int M, N, K;
+  // EPI_SWIGLU_BWD: [a; b] rows (fp32, 2I per row) in, [da; db] and h (bf16) out
+  const float* AB;
+  uint16_t* dA13;
+  uint16_t* Hh;
+  int I;
+};
+
+// LDS position of 16-byte chunk c of operand row r: XOR-swizzled by the row's low and
+// next three bits, so that 16 consecutive rows read at one chunk and the transposed
+// stores of 16 rows eight apart both spread over the bank groups.
+__device__ __forceinline__ int lds_pos(int r, int c) {
+  return r * ROWB + ((c ^ (r & 7) ^ ((r >> 3) & 7)) << 4);
+}
+
+template <bool TA, bool TB, bool KROWS, int EPI>
+__global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2][2][OPB];
+  __shared__ int s_cum[MAXG + 1];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves of 64 x 64
+  const int ng = p.g_end - p.g_begin;
+  const int ntn = p.N / TN;
+
+  // tile index with consecutive indices on one XCD (blocks are dealt round-robin)
+  const int per = (int)gridDim.x >> 3;
+  const int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  int g, m0, n0, Kg, base, rows;
+  if (KROWS) {
+    const int tpg = (p.M / TM) * ntn;
+    if (L >= ng * tpg) return;
+    const int gi = L / tpg, loc = L - gi * tpg;
+    g = p.g_begin + gi;
+    m0 = (loc / ntn) * TM;
+    n0 = (loc % ntn) * TN;
+    Kg = p.count[g];
+    base = p.offset[g];
+    rows = TM;
+  } else {
+    if (tid < 64) {
+      int running = 0;
+      for (int i0 = 0; i0 < ng; i0 += 64) {
+        const int i = i0 + tid;
+        const int nt = i < ng ? ((p.count[p.g_begin + i] + TM - 1) / TM) * ntn : 0;
+        const int incl = wave_incl_scan(nt);
+        if (i < ng) s_cum[i + 1] = running + incl;
+        running += __shfl(incl, 63, 64);
+      }
+      if (tid == 0) s_cum[0] = 0;
+    }
+    __syncthreads();
+    if (L >= s_cum[ng]) return;
+    int lo = 0, hi = ng - 1;  // last group with s_cum[i] <= L
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_cum[mid] <= L) lo = mid; else hi = mid - 1;
+    }
+    g = p.g_begin + lo;
+    const int cnt = p.count[g];
+    const int mt = (cnt + TM - 1) / TM;
+    const int loc = L - s_cum[lo];
+    n0 = (loc / mt) * TN;
+    m0 = (loc % mt) * TM;
+    rows = min(TM, cnt - m0);
+    base = p.offset[g] + m0;
+    Kg = p.K;
+  }
+  const uint16_t* Bg = p.B;
+  if (!KROWS) Bg = (g < p.n_pub) ? p.B + (size_t)g * p.strideB : p.B_priv + (size_t)(g - p.n_pub) * p.strideB;
+
+  u32x4 ra[4], rb[4];
+  // Registers of K step k0: direct operands 4 x 16 bytes of rows (t + 256 i) / 8,
+  // transposed operands 4 consecutive K rows x 8 columns.
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (!TA) {
+        const int q = tid + BT * i, r = q >> 3, c = q & 7;
+        const int rr = min(r, rows - 1);
+        ra[i] = *(const u32x4*)(p.A + (size_t)(base + rr) * p.lda + k0 + c * 8);
+      } else {
+        const int kk = k0 + (tid >> 4) * 4 + i, col = m0 + (tid & 15) * 8;
+        const int kc = min(kk, Kg - 1);
+        u32x4 v = *(const u32x4*)(p.A + (size_t)(base + kc) * p.lda + col);
+        ra[i] = kk < Kg ? v : u32x4{0, 0, 0, 0};
+      }
+      if (!TB) {
+        const int q = tid + BT * i, r = q >> 3, c = q & 7;
+        rb[i] = *(const u32x4*)(Bg + (size_t)(n0 + r) * p.ldb + k0 + c * 8);
+      } else {
+        const int kk = k0 + (tid >> 4) * 4 + i, col = n0 + (tid & 15) * 8;
+        if (KROWS) {
+          const int kc = min(kk, Kg - 1);
+          u32x4 v = *(const u32x4*)(Bg + (size_t)(base + kc) * p.ldb + col);
+          rb[i] = kk < Kg ? v : u32x4{0, 0, 0, 0};
+        } else {
+          rb[i] = *(const u32x4*)(Bg + (size_t)kk * p.ldb + col);
+        }
+      }
+    }
+  };
+  auto store_op = [&](unsigned char* dst, const u32x4 (&v)[4], bool transposed) {
+    if (!transposed) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = tid + BT * i;
+        *(u32x4*)(dst + lds_pos(q >> 3, q & 7)) = v[i];
+      }
+    } else {
+      const int kg = tid >> 4, r0 = (tid & 15) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int w = j >> 1;
+        uint32_t d0, d1;
+        if (j & 1) {
+          d0 = (v[0][w] >> 16) | (v[1][w] & 0xFFFF0000u);
+          d1 = (v[2][w] >> 16) | (v[3][w] & 0xFFFF0000u);
+        } else {
+          d0 = (v[0][w] & 0xFFFFu) | (v[1][w] << 16);
+          d1 = (v[2][w] & 0xFFFFu) | (v[3][w] << 16);
+        }
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        *(u32x2*)(dst + lds_pos(r0 + j, kg >> 1) + (kg & 1) * 8) = u32x2{d0, d1};
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+    store_op(smem[buf][0], ra, TA);
+    store_op(smem[buf][1], rb, TB);
+  };
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+
+  const int nk = (Kg + TK - 1) / TK;
+  if (nk > 0) {
+    gload(0);
+    lstore(0);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    gload(min(kt + 1, nk - 1) * TK);  // the last step reloads itself; its store is unused
+#pragma unroll
+    for (int sub = 0; sub < TK / 32; ++sub) {
+      const int ch = sub * 4 + (lane >> 4);
+      bf16x8 fa[4], fb[4];
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+        fa[mb] = as_bf16x8(*(const u32x4*)(smem[cur][0] + lds_pos(wm * 64 + mb * 16 + (lane & 15), ch)));
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+        fb[nb] = as_bf16x8(*(const u32x4*)(smem[cur][1] + lds_pos(wn * 64 + nb * 16 + (lane & 15), ch)));
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+    }
+    lstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue: lane holds C[m = 4 (lane / 16) + i][n = lane % 16] of each 16 x 16 block.
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = wm * 64 + mb * 16 + (lane >> 4) * 4 + i;
+      if (m >= rows) continue;
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const int n = n0 + wn * 64 + nb * 16 + (lane & 15);
+        const float v = acc[mb][nb][i];
+        if (EPI == EPI_F32) {
+          if (KROWS)
+            p.C[(size_t)(g - p.g_begin) * p.strideC + (size_t)(m0 + m) * p.ldc + n] = v;
+          else
+            p.C[(size_t)(base + m) * p.ldc + n] = v;
+        } else {
+          const size_t r = (size_t)(base + m);
+          const float ga = p.AB[r * 2 * p.I + n], ub = p.AB[r * 2 * p.I + p.I + n];
+          const float s = 1.0f / (1.0f + __expf(-ga));
+          const float da = v * ub * s * (1.0f + ga * (1.0f - s));
+          const float db = v * ga * s;
+          p.dA13[r * 2 * p.I + n] = (uint16_t)f32_to_bf16_rne(da);
+          p.dA13[r * 2 * p.I + p.I + n] = (uint16_t)f32_to_bf16_rne(db);
+          p.Hh[r * p.I + n] = (uint16_t)f32_to_bf16_rne(ga * s * ub);
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Reductions
+// ---------------------------------------------------------------------------
+// dx_t = sum_j (dXr[r_j] + dz_j W_r[e_j]) in slot order, four columns per thread.
+__global__ __launch_bounds__(BT) void bwd_dx_kernel(BwdArgs a) {
+  __shared__ int s_r[PMPE_MAX_TOPK];
+  __shared__ const float* s_w[PMPE_MAX_TOPK];
+  __shared__ float s_dz[PMPE_MAX_TOPK];
+  const int t = blockIdx.x, H = a.H, k = a.k, tid = threadIdx.x;
+  if (tid < k) {
+    const int r = a.token_row[t * k + tid], e = a.topk_idx[t * k + tid];
+    s_r[tid] = r;
+    s_dz[tid] = a.dz_row[r];
+    s_w[tid] = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
+  }
+  __syncthreads();
+  for (int h = tid * 4; h < H; h += BT * 4) {
+    f32x4 s = {0, 0, 0, 0};
+    for (int j = 0; j < k; ++j) {
+      const f32x4 d = *(const f32x4*)(a.dXr + (size_t)s_r[j] * H + h);
+      const f32x4 w = *(const f32x4*)(s_w[j] + h);
+      s += d + s_dz[j] * w;
+    }
+    *(f32x4*)(a.dx + (size_t)t * H + h) = s;
+  }
+}
+
+// Router-row gradient of private expert p, in two fixed-order stages: block (p, c) sums
+// dz_r Xp[r] over the c-th of BWD_DWR_SPLIT equal chunks of p's rows (ascending), eight
+// columns per thread; then dW_r[p] = sum over the chunks in order. grad_rows[p] = rows.
+__global__ __launch_bounds__(BT) void bwd_dwr_part_kernel(BwdArgs a) {
+  const int pe = blockIdx.x, c = blockIdx.y, e = a.n_pub + pe, H = a.H;
+  const int cnt = a.count[e], off = a.offset[e];
+  if (c == 0 && threadIdx.x == 0 && a.grad_rows) a.grad_rows[pe] = (uint32_t)cnt;
+  const int per = (cnt + BWD_DWR_SPLIT - 1) / BWD_DWR_SPLIT;
+  const int r0 = off + min(cnt, c * per), r1 = off + min(cnt, (c + 1) * per);
+  float* part = a.dwr_part + ((size_t)pe * BWD_DWR_SPLIT + c) * H;
+  for (int h = threadIdx.x * 8; h < H; h += BT * 8) {
+    float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int r = r0; r < r1; ++r) {
+      const u32x4 v = *(const u32x4*)(a.Xp + (size_t)r * H + h);
+      const float dz = a.dz_row[r];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        s[2 * q] += dz * bf16_to_f32(v[q] & 0xFFFFu);
+        s[2 * q + 1] += dz * bf16_to_f32(v[q] >> 16);
+      }
+    }
+    *(f32x4*)(part + h) = f32x4{s[0], s[1], s[2], s[3]};
+    *(f32x4*)(part + h + 4) = f32x4{s[4], s[5], s[6], s[7]};
+  }
+}
+
+__global__ __launch_bounds__(BT) void bwd_dwr_sum_kernel(BwdArgs a) {
+  const int pe = blockIdx.y, H = a.H;
+  const int h = blockIdx.x * BT + threadIdx.x;
+  if (h >= H) return;
+  float s = 0.f;
+  for (int c = 0; c < BWD_DWR_SPLIT; ++c) s += a.dwr_part[((size_t)pe * BWD_DWR_SPLIT + c) * H + h];
+  a.dwr_priv[(size_t)pe * H + h] = s;
+}
+
+template <bool TA, bool TB, bool KROWS, int EPI>
+hipError_t launch_gemm(const GemmArgs& g, int tiles, hipStream_t s) {
+  if (tiles <= 0) return hipSuccess;
+  const int grid = (tiles + 7) / 8 * 8;
+  bwd_gemm_kernel<TA, TB, KROWS, EPI><<<grid, BT, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
+  const int E = a.n_pub + a.n_priv, H = a.H, I = a.I, R = a.T * a.k;
+  bwd_rows_kernel<<<a.T, BT, 0, s>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // ROWS launches: at most R / TM + E row tiles over all groups
+  const int mt_max = R / TM + E;
+  GemmArgs g{};
+  g.count = a.count;
+  g.offset = a.offset;
+  g.n_pub = a.n_pub;
+  g.I = I;
+  g.g_begin = 0;
+  g.g_end = E;
+  const float* AB = a.ab;
+  if (!AB) {
+    // [a; b] = Xp W13^T over every executed expert (not saved by the forward)
+    g.A = a.Xp; g.lda = H;
+    g.B = (const uint16_t*)a.w13_pub; g.B_priv = (const uint16_t*)a.w13_priv;
+    g.strideB = (size_t)2 * I * H; g.ldb = H;
+    g.C = a.AB; g.ldc = 2 * I;
+    g.N = 2 * I; g.K = H;
+    e = launch_gemm<false, false, false, EPI_F32>(g, mt_max * (g.N / TN), s);
+    if (e != hipSuccess) return e;
+    AB = a.AB;
+  }
+  // dh = dY W2 (W2 stored [H, I]: K rows of N columns), SwiGLU backward in the epilogue
+  g.A = a.dY; g.lda = H;
+  g.B = (const uint16_t*)a.w2_pub; g.B_priv = (const uint16_t*)a.w2_priv;
+  g.strideB = (size_t)H * I; g.ldb = I;
+  g.C = nullptr; g.N = I; g.K = H;
+  g.AB = AB; g.dA13 = a.dA13; g.Hh = a.Hh;
+  e = launch_gemm<false, true, false, EPI_SWIGLU_BWD>(g, mt_max * (g.N / TN), s);
+  if (e != hipSuccess) return e;
+  // dXr = [da; db] W13 (W13 stored [2I, H])
+  g.A = a.dA13; g.lda = 2 * I;
+  g.B = (const uint16_t*)a.w13_pub; g.B_priv = (const uint16_t*)a.w13_priv;
+  g.strideB = (size_t)2 * I * H; g.ldb = H;
+  g.C = a.dXr; g.ldc = H; g.N = H; g.K = 2 * I;
+  e = launch_gemm<false, true, false, EPI_F32>(g, mt_max * (g.N / TN), s);
+  if (e != hipSuccess) return e;
+  if (a.n_priv > 0) {
+    // dW2[p] = dY^T Hh over private expert p's rows: M = H, N = I
+    GemmArgs w{};
+    w.count = a.count; w.offset = a.offset; w.n_pub = a.n_pub;
+    w.g_begin = a.n_pub; w.g_end = E;
+    w.A = a.dY; w.lda = H; w.B = a.Hh; w.ldb = I;
+    w.C = a.dw2_priv; w.ldc = I; w.strideC = (size_t)H * I; w.M = H; w.N = I;
+    e = launch_gemm<true, true, true, EPI_F32>(w, a.n_priv * (H / TM) * (I / TN), s);
+    if (e != hipSuccess) return e;
+    // dW13[p] = [da; db]^T Xp: M = 2I, N = H
+    w.A = a.dA13; w.lda = 2 * I; w.B = a.Xp; w.ldb = H;
+    w.C = a.dw13_priv; w.ldc = H; w.strideC = (size_t)2 * I * H; w.M = 2 * I; w.N = H;
+    e = launch_gemm<true, true, true, EPI_F32>(w, a.n_priv * (2 * I / TM) * (H / TN), s);
+    if (e != hipSuccess) return e;
+    bwd_dwr_part_kernel<<<dim3(a.n_priv, BWD_DWR_SPLIT), BT, 0, s>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    bwd_dwr_sum_kernel<<<dim3((H + BT - 1) / BT, a.n_priv), BT, 0, s>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  bwd_dx_kernel<<<a.T, BT, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace pmpe

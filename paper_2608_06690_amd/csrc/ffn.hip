@@ -194,7 +194,9 @@ struct TileInfo {
 // tile's last MFMAs and its epilogue. Gather indices (row_token slices) are fetched by
 // LDS-DMA as well, one tile ahead of their use, so no register-destined global load
 // inside the stream forces the compiler to drain the ring.
-template <class C, bool GATED>
+// SAVE (GEMM1 only): also store the fp32 gate and up projections [a; b] of every routed
+// row into ab_save [T*k, 2I], for a later backward pass.
+template <class C, bool GATED, bool SAVE = false>
 __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
   __shared__ __attribute__((aligned(16))) int s_rt[3][C::BM];
@@ -481,6 +483,15 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
               const int c = wn * WCOLS + nb * 16 + (lane & 15);
               const float v = GATED ? silu(acc[mb][nb][i]) * acc[mb][nb + NBO][i] : acc[mb][nb][i];
               so[r * NCOLS + c] = (uint16_t)f32_to_bf16_rne(v);
+              if constexpr (GATED && SAVE) {
+                const int rt = r0 + (lane >> 4) * 4 + i;  // row within the tile
+                const int col = ct.n0 + c;
+                if (ct.g < E && rt < ct.rows && col < width) {
+                  float* ab = a.ab_save + (size_t)(ct.base + rt) * (2 * width);
+                  ab[col] = acc[mb][nb][i];
+                  ab[width + col] = acc[mb][nb + NBO][i];
+                }
+              }
             }
         }
       }
@@ -721,11 +732,17 @@ hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) {
     };
     if (large) {
       using C = CfgLarge;
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      if (a.ab_save)
+        hipLaunchKernelGGL((gemm_bf16_kernel<C, true, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      else
+        hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
       hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
     } else {
       using C = CfgSmall;
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      if (a.ab_save)
+        hipLaunchKernelGGL((gemm_bf16_kernel<C, true, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      else
+        hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
       hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
     }
   } else {

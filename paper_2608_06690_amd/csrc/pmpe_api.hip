@@ -72,6 +72,35 @@ size_t ffn_ws(const pmpe_layer_desc* d, int32_t T) {
 
 pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR_LAUNCH; }
 
+// backward workspace: Xp, dY, [a; b], h, [da; db], row input gradients, row dz
+struct BwdLayout {
+  size_t xp, dy, ab, hh, da, dxr, dz, part, total;
+};
+BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
+  const size_t R = (size_t)T * d->top_k, H = d->hidden, I = d->inter;
+  BwdLayout L;
+  size_t o = 0;
+  L.xp = o; o += round_up(R * H * 2);
+  L.dy = o; o += round_up(R * H * 2);
+  L.ab = o; o += round_up(R * 2 * I * 4);
+  L.hh = o; o += round_up(R * I * 2);
+  L.da = o; o += round_up(R * 2 * I * 2);
+  L.dxr = o; o += round_up(R * H * 4);
+  L.dz = o; o += round_up(R * 4);
+  L.part = o; o += round_up((size_t)d->n_priv * BWD_DWR_SPLIT * H * 4);
+  L.total = o;
+  return L;
+}
+
+pmpe_status check_backward_desc(const pmpe_layer_desc* d, int32_t T) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (d->act_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
+  if (d->gate_mode != PMPE_GATE_RENORM_TOPK || d->n_shared != 0 || d->inter % 128 != 0)
+    return PMPE_ERR_SHAPE;
+  return PMPE_OK;
+}
+
 // two ping-pong digest arrays: every level fits in the one it does not read
 size_t fingerprint_ws_parts(uint64_t nbytes, size_t* part0) {
   const uint64_t n = fingerprint_leaves(nbytes);
@@ -81,6 +110,40 @@ size_t fingerprint_ws_parts(uint64_t nbytes, size_t* part0) {
   }
   *part0 = round_up((size_t)n * 32);
   return *part0 + round_up((size_t)((n + kFpFanout - 1) / kFpFanout) * 32);
+}
+
+pmpe_status expert_ffn_impl(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                            const void* x, const int32_t* expert_count,
+                            const int32_t* expert_offset, const int32_t* row_token,
+                            const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                            const void* w2_priv, const void* w13_sh, const void* w2_sh,
+                            void* y_shared, void* y_perm, uint32_t* audit_token_rows,
+                            uint32_t* audit_priv_calls, uint32_t* dev_status, void* ws,
+                            size_t ws_bytes, pmpe_stream_t stream, float* ab_save) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (!expert_count || !expert_offset || !row_token || !w13_pub || !w2_pub || !y_perm ||
+      !audit_token_rows)
+    return PMPE_ERR_NULL;
+  if (!x_perm && !x) return PMPE_ERR_NULL;
+  if (d->n_shared > 0 && (!x || !w13_sh || !w2_sh || !y_shared)) return PMPE_ERR_NULL;
+  const void* al[] = {x_perm, x, w13_pub, w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
+  if (ab_save && d->act_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
+  if (ab_save && !aligned16(ab_save)) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  if (!ws || ws_bytes < ffn_ws(d, T)) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  const size_t el = elem_bytes(d);
+  const int Is = d->n_shared * d->shared_inter;
+  void* h = ws;
+  void* h_sh = (char*)ws + round_up((size_t)T * d->top_k * d->inter * el);
+  FfnArgs a{T, d->hidden, d->inter, d->n_pub, d->n_priv, d->top_k, d->act_dtype == PMPE_BF16,
+            d->n_shared > 0 ? Is : 0, x_perm, x, expert_count, expert_offset, row_token,
+            w13_pub, w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm,
+            audit_token_rows, audit_priv_calls, dev_status, h, h_sh, ab_save};
+  return launched(launch_expert_ffn(a, (hipStream_t)stream));
 }
 
 }  // namespace
@@ -160,28 +223,23 @@ pmpe_status pmpe_expert_ffn(const pmpe_layer_desc* d, int32_t T, const void* x_p
                             void* y_shared, void* y_perm, uint32_t* audit_token_rows,
                             uint32_t* audit_priv_calls, uint32_t* dev_status, void* ws,
                             size_t ws_bytes, pmpe_stream_t stream) {
-  pmpe_status st = check_desc(d, T);
-  if (st != PMPE_OK) return st;
-  if (!expert_count || !expert_offset || !row_token || !w13_pub || !w2_pub || !y_perm ||
-      !audit_token_rows)
-    return PMPE_ERR_NULL;
-  if (!x_perm && !x) return PMPE_ERR_NULL;
-  if (d->n_shared > 0 && (!x || !w13_sh || !w2_sh || !y_shared)) return PMPE_ERR_NULL;
-  const void* al[] = {x_perm, x, w13_pub, w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm};
-  for (const void* p : al)
-    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
-  if (T == 0) return PMPE_OK;
-  if (!ws || ws_bytes < ffn_ws(d, T)) return PMPE_ERR_WORKSPACE;
-  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
-  const size_t el = elem_bytes(d);
-  const int Is = d->n_shared * d->shared_inter;
-  void* h = ws;
-  void* h_sh = (char*)ws + round_up((size_t)T * d->top_k * d->inter * el);
-  FfnArgs a{T, d->hidden, d->inter, d->n_pub, d->n_priv, d->top_k, d->act_dtype == PMPE_BF16,
-            d->n_shared > 0 ? Is : 0, x_perm, x, expert_count, expert_offset, row_token,
-            w13_pub, w2_pub, w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm,
-            audit_token_rows, audit_priv_calls, dev_status, h, h_sh};
-  return launched(launch_expert_ffn(a, (hipStream_t)stream));
+  return expert_ffn_impl(d, T, x_perm, x, expert_count, expert_offset, row_token, w13_pub, w2_pub,
+                         w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm, audit_token_rows,
+                         audit_priv_calls, dev_status, ws, ws_bytes, stream, nullptr);
+}
+
+pmpe_status pmpe_expert_ffn_train(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                                  const void* x, const int32_t* expert_count,
+                                  const int32_t* expert_offset, const int32_t* row_token,
+                                  const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                                  const void* w2_priv, const void* w13_sh, const void* w2_sh,
+                                  void* y_shared, void* y_perm, uint32_t* audit_token_rows,
+                                  uint32_t* audit_priv_calls, uint32_t* dev_status, float* ab,
+                                  void* ws, size_t ws_bytes, pmpe_stream_t stream) {
+  if (!ab) return PMPE_ERR_NULL;
+  return expert_ffn_impl(d, T, x_perm, x, expert_count, expert_offset, row_token, w13_pub, w2_pub,
+                         w13_priv, w2_priv, w13_sh, w2_sh, y_shared, y_perm, audit_token_rows,
+                         audit_priv_calls, dev_status, ws, ws_bytes, stream, ab);
 }
 
 pmpe_status pmpe_combine(const pmpe_layer_desc* d, int32_t T, const void* y_perm,
@@ -211,6 +269,43 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
   AuditArgs a{T, R, audit_token_rows, allow, req_offset, req_private_rows, total_private_rows,
               deny_violations};
   return launched(launch_audit(a, (hipStream_t)stream));
+}
+
+size_t pmpe_backward_workspace_bytes(const pmpe_layer_desc* d, int32_t T) {
+  if (check_backward_desc(d, T) != PMPE_OK) return 0;
+  return bwd_layout(d, T).total;
+}
+
+pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, const void* dout,
+                          const int32_t* topk_idx, const float* topk_gate,
+                          const int32_t* expert_count, const int32_t* expert_offset,
+                          const int32_t* row_token, const int32_t* token_row, const void* y_perm,
+                          const float* wr_pub, const float* wr_priv, const void* w13_pub,
+                          const void* w2_pub, const void* w13_priv, const void* w2_priv,
+                          const float* ab, float* dx, float* dw13_priv, float* dw2_priv,
+                          float* dwr_priv, uint32_t* grad_rows, void* ws, size_t ws_bytes,
+                          pmpe_stream_t stream) {
+  pmpe_status st = check_backward_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (!x || !dout || !topk_idx || !topk_gate || !expert_count || !expert_offset || !row_token ||
+      !token_row || !y_perm || !wr_pub || !w13_pub || !w2_pub || !dx)
+    return PMPE_ERR_NULL;
+  if (d->n_priv > 0 && (!wr_priv || !w13_priv || !w2_priv || !dw13_priv || !dw2_priv || !dwr_priv))
+    return PMPE_ERR_NULL;
+  const void* al[] = {x, dout, y_perm, w13_pub, w2_pub, w13_priv, w2_priv, ab};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  const BwdLayout L = bwd_layout(d, T);
+  if (!ws || ws_bytes < L.total) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  char* w = (char*)ws;
+  BwdArgs a{T, d->hidden, d->inter, d->top_k, d->n_pub, d->n_priv, x, dout, topk_idx, topk_gate,
+            expert_count, expert_offset, row_token, token_row, y_perm, wr_pub, wr_priv, w13_pub,
+            w2_pub, w13_priv, w2_priv, ab, dx, dw13_priv, dw2_priv, dwr_priv, grad_rows,
+            (uint16_t*)(w + L.xp), (uint16_t*)(w + L.dy), (float*)(w + L.ab), (uint16_t*)(w + L.hh),
+            (uint16_t*)(w + L.da), (float*)(w + L.dxr), (float*)(w + L.dz), (float*)(w + L.part)};
+  return launched(launch_backward(a, (hipStream_t)stream));
 }
 
 size_t pmpe_fingerprint_workspace_bytes(uint64_t nbytes) {

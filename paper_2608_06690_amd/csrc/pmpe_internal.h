@@ -128,6 +128,7 @@ struct FfnArgs {
   uint32_t* dev_status;
   void* h;     // workspace [T*k, I]
   void* h_sh;  // workspace [T, Is]
+  float* ab_save = nullptr;  // optional [T*k, 2I]: fp32 gate and up projections (bf16 path)
 };
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 
@@ -151,6 +152,43 @@ struct AuditArgs {
   uint32_t* violations;
 };
 hipError_t launch_audit(const AuditArgs& a, hipStream_t s);
+
+struct BwdArgs {
+  int T, H, I, k, n_pub, n_priv;
+  const void* x;          // [T, H] bf16
+  const void* dout;       // [T, H] bf16
+  const int32_t* topk_idx;
+  const float* topk_gate;
+  const int32_t* count;
+  const int32_t* offset;
+  const int32_t* row_token;
+  const int32_t* token_row;
+  const void* y_perm;     // [T*k, H] bf16
+  const float* wr_pub;
+  const float* wr_priv;
+  const void* w13_pub;
+  const void* w2_pub;
+  const void* w13_priv;
+  const void* w2_priv;
+  const float* ab;        // [T*k, 2I] saved by the forward, or NULL: recomputed into AB
+  float* dx;
+  float* dw13_priv;
+  float* dw2_priv;
+  float* dwr_priv;
+  uint32_t* grad_rows;
+  // workspace
+  uint16_t* Xp;    // [T*k, H]
+  uint16_t* dY;    // [T*k, H]
+  float* AB;       // [T*k, 2I]
+  uint16_t* Hh;    // [T*k, I]
+  uint16_t* dA13;  // [T*k, 2I]
+  float* dXr;      // [T*k, H]
+  float* dz_row;   // [T*k]
+  float* dwr_part; // [n_priv, BWD_DWR_SPLIT, H]
+};
+constexpr int BWD_DWR_SPLIT = 16;  // row chunks per private expert in the router-row gradient
+
+hipError_t launch_backward(const BwdArgs& a, hipStream_t s);
 
 // Fingerprint tree: 1 KiB leaves, 16 digests per inner node.
 constexpr uint32_t kFpLeafBytes = 1024;

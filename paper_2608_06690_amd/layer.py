@@ -27,6 +27,17 @@ class LayerBuffers:
     out: torch.Tensor
     ws: torch.Tensor
     dev_status: torch.Tensor
+    ab: Optional[torch.Tensor] = None   # [T*k, 2I] fp32, filled by a training forward
+
+
+@dataclasses.dataclass
+class GradBuffers:
+    dx: torch.Tensor                    # [T, H] fp32
+    dw13_priv: Optional[torch.Tensor]   # [n_priv, 2I, H] fp32
+    dw2_priv: Optional[torch.Tensor]    # [n_priv, H, I] fp32
+    dwr_priv: Optional[torch.Tensor]    # [n_priv, H] fp32
+    grad_rows: torch.Tensor             # [n_priv] uint32 (int32 storage)
+    ws: torch.Tensor
 
 
 @dataclasses.dataclass
@@ -109,8 +120,18 @@ class PolicyMaskedMoE:
         N.pmpe_dispatch(self.desc, T, b.topk_idx, x, b.expert_count, b.expert_offset, b.row_token,
                         b.token_row, b.x_perm, b.ws, stream)
 
-    def expert_ffn(self, x, b: LayerBuffers, audit: AuditBuffers, stream=None):
+    def expert_ffn(self, x, b: LayerBuffers, audit: AuditBuffers, stream=None, train=False):
         T = x.shape[0]
+        if train:
+            if b.ab is None:
+                b.ab = torch.empty(T * self.desc.top_k, 2 * self.desc.inter, dtype=torch.float32,
+                                   device=self.device)
+            N.pmpe_expert_ffn_train(
+                self.desc, T, b.x_perm, x, b.expert_count, b.expert_offset, b.row_token,
+                self.w13_pub, self.w2_pub, self.w13_priv, self.w2_priv, self.w13_sh, self.w2_sh,
+                b.y_shared, b.y_perm, audit.token_rows, audit.priv_calls, b.dev_status, b.ab, b.ws,
+                stream)
+            return
         N.pmpe_expert_ffn(self.desc, T, b.x_perm, x, b.expert_count, b.expert_offset, b.row_token,
                           self.w13_pub, self.w2_pub, self.w13_priv, self.w2_priv, self.w13_sh,
                           self.w2_sh, b.y_shared, b.y_perm, audit.token_rows, audit.priv_calls,
@@ -125,12 +146,39 @@ class PolicyMaskedMoE:
         N.pmpe_audit(self.desc, T, audit.token_rows, b.allow, req_offset, R, audit.req_rows,
                      audit.total, audit.violations, stream)
 
-    def forward(self, x, words, audit: AuditBuffers, req_offset=None, stream=None) -> LayerBuffers:
-        """Runs the layer; returns the buffers (out, route log, dispatch) of this T."""
+    def grad_buffers(self, T: int) -> GradBuffers:
+        d, dev, H, I, P = self.desc, self.device, self.desc.hidden, self.desc.inter, self.desc.n_priv
+        f32 = dict(dtype=torch.float32, device=dev)
+        return GradBuffers(torch.empty(T, H, **f32),
+                           torch.empty(P, 2 * I, H, **f32) if P else None,
+                           torch.empty(P, H, I, **f32) if P else None,
+                           torch.empty(P, H, **f32) if P else None,
+                           torch.zeros(max(P, 1), dtype=torch.int32, device=dev),
+                           torch.empty(max(N.pmpe_backward_workspace_bytes(d, T), 256),
+                                       dtype=torch.uint8, device=dev))
+
+    def backward(self, x, dout, b: LayerBuffers, g: Optional[GradBuffers] = None,
+                 stream=None, use_saved: bool = True) -> GradBuffers:
+        """Private-only backward of the forward that filled `b` (same x): input gradient
+        and the gradients of the private experts and private router rows. The gate and
+        up projections saved by a training forward are used when present (and
+        `use_saved`), else recomputed."""
+        T = x.shape[0]
+        g = g or self.grad_buffers(T)
+        N.pmpe_backward(self.desc, T, x, dout, b.topk_idx, b.topk_gate, b.expert_count,
+                        b.expert_offset, b.row_token, b.token_row, b.y_perm, self.wr_pub,
+                        self.wr_priv, self.w13_pub, self.w2_pub, self.w13_priv, self.w2_priv,
+                        b.ab if use_saved else None, g.dx, g.dw13_priv, g.dw2_priv, g.dwr_priv, g.grad_rows, g.ws, stream)
+        return g
+
+    def forward(self, x, words, audit: AuditBuffers, req_offset=None, stream=None,
+                train: bool = False) -> LayerBuffers:
+        """Runs the layer; returns the buffers (out, route log, dispatch) of this T. A
+        training forward also keeps what the backward needs (b.ab)."""
         b = self.buffers(x.shape[0])
         self.route(x, words, b, stream)
         self.dispatch(x, b, stream)
-        self.expert_ffn(x, b, audit, stream)
+        self.expert_ffn(x, b, audit, stream, train)
         self.combine(x, b, stream)
         if req_offset is not None:
             self.audit(x.shape[0], b, audit, req_offset, stream)

@@ -204,7 +204,7 @@ def normal(key: int, shape: Sequence[int], std: float, dtype: torch.dtype = torc
 
 
 # tensor ids inside a layer's key space
-T_X, T_WR_PUB, T_WR_PRIV, T_BIAS, T_W13_PUB, T_W2_PUB, T_W13_PRIV, T_W2_PRIV, T_W13_SH, T_W2_SH = range(10)
+T_X, T_WR_PUB, T_WR_PRIV, T_BIAS, T_W13_PUB, T_W2_PUB, T_W13_PRIV, T_W2_PRIV, T_W13_SH, T_W2_SH, T_DOUT = range(11)
 
 
 def torch_dtype(cfg: LayerConfig) -> torch.dtype:
@@ -237,6 +237,12 @@ def make_x(cfg: LayerConfig, device="cpu", tokens: Optional[Sequence[int]] = Non
     x = normal(tensor_key(cfg.seed, 0, T_X, 0), (cfg.tokens, cfg.hidden), cfg.x_std,
                torch_dtype(cfg), device)
     return x if tokens is None else x[torch.as_tensor(tokens, device=x.device)]
+
+
+def make_dout(cfg: LayerConfig, layer: int = 0, device="cpu", std: float = 1.0) -> torch.Tensor:
+    """Upstream gradient of the layer output, [T, H] in the activation dtype."""
+    return normal(tensor_key(cfg.seed, layer, T_DOUT, 0), (cfg.tokens, cfg.hidden), std,
+                  torch_dtype(cfg), device)
 
 
 def make_router(cfg: LayerConfig, layer: int = 0, device="cpu"):
