@@ -57,7 +57,8 @@ typedef enum {
   PMPE_ERR_DTYPE = -4,           /* unsupported dtype combination */
   PMPE_ERR_ALIGN = -5,           /* a pointer is not 16-byte aligned */
   PMPE_ERR_WORKSPACE = -6,       /* workspace missing or smaller than pmpe_workspace_bytes */
-  PMPE_ERR_LAUNCH = -7           /* the HIP runtime refused a launch */
+  PMPE_ERR_LAUNCH = -7,          /* the HIP runtime refused a launch */
+  PMPE_ERR_TAG_MISMATCH = -8     /* a cache tag does not match the request (reuse refused) */
 } pmpe_status;
 
 typedef enum { PMPE_F32 = 0, PMPE_BF16 = 1 } pmpe_dtype;
@@ -272,6 +273,53 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
                        const uint8_t* allow, const int32_t* req_offset, int32_t R,
                        uint64_t* req_private_rows, uint64_t* total_private_rows,
                        uint32_t* deny_violations, pmpe_stream_t stream);
+
+/*
+ * pmpe_route_record - export the route audit of one layer call: one record per token
+ * with the layer, the request row, the token's position in the request, the selected
+ * pool and the policy decision (App. B.1, fifth step of the fail-closed request
+ * procedure; App. B.2: route counters are indexed by row and layer, so a batch total
+ * cannot hide cross-row leakage). The records come from the route log (topk_idx,
+ * allow), not from the expert kernels, so they can be reconciled against the
+ * independent execution counters of pmpe_expert_ffn / pmpe_audit.
+ *
+ *   layer        layer index written into every record (0..65535)
+ *   topk_idx     [T*k], allow [T]        from pmpe_route
+ *   req_offset   [R + 1] device, as in pmpe_audit (R >= 1 when T > 0)
+ *   rec          [T] pmpe_route_rec out, 16-byte aligned
+ */
+#define PMPE_POOL_PUBLIC 0u  /* every selected expert is public */
+#define PMPE_POOL_PRIVATE 1u /* every selected expert is private */
+#define PMPE_POOL_MIXED 2u   /* both (only the soft-routing control can do this) */
+typedef struct {
+  uint32_t layer_decision_pool; /* bits 0-15 layer, bit 16 decision (1 allow), bits 24-31 pool */
+  int32_t row;                  /* request (batch row) index */
+  int32_t token;                /* position of the token in its request */
+  uint32_t private_mask;        /* bit j: the expert in slot j (ascending ids) is private */
+} pmpe_route_rec;
+
+pmpe_status pmpe_route_record(const pmpe_layer_desc* d, int32_t T, int32_t layer,
+                              const int32_t* topk_idx, const uint8_t* allow,
+                              const int32_t* req_offset, int32_t R, pmpe_route_rec* rec,
+                              pmpe_stream_t stream);
+
+/*
+ * pmpe_cache_tag_check - host-side guard for cached attention state (App. B.1, third
+ * step of the fail-closed request procedure; App. B.2: caches are tagged with the
+ * policy decision, the model revision and the checkpoint fingerprint, and reuse across
+ * tags is refused before a model call).
+ *
+ * Returns PMPE_OK only when both tags are present, both decisions are well formed (0
+ * deny or 1 allow) and every field is equal; PMPE_ERR_TAG_MISMATCH otherwise (a missing
+ * or malformed tag is refused, never treated as a match). Host pointers; no GPU work.
+ */
+typedef struct {
+  uint32_t decision;                 /* resolved policy of the request: 1 allow, 0 deny */
+  uint8_t model_revision[32];        /* e.g. SHA-256 of the model revision string */
+  uint8_t checkpoint_fingerprint[32]; /* pmpe_fingerprint of the loaded weights */
+} pmpe_cache_tag;
+
+pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_tag* request);
 
 /*
  * pmpe_backward - private-only backward of one layer for an upstream gradient dout.

@@ -531,3 +531,36 @@ def fingerprint_set(parts: Sequence[bytes]) -> bytes:
     """Fingerprint of several buffers: the fingerprint of the concatenation of their
     fingerprints, in order."""
     return fingerprint(b"".join(fingerprint(p) for p in parts))
+
+
+# ----------------------------------------------------------------------------
+# Route records and cache tags (App. B.1 fail-closed request procedure, steps 3 and 5;
+# App. B.2 state isolation and cache discipline)
+# ----------------------------------------------------------------------------
+
+POOL_PUBLIC, POOL_PRIVATE, POOL_MIXED = 0, 1, 2
+
+
+def route_records(idx: np.ndarray, allow: np.ndarray, req_offset: Sequence[int], n_pub: int,
+                  layer: int) -> np.ndarray:
+    """One record per token: (layer | decision << 16 | pool << 24, request row, position in
+    the request, mask of the slots whose selected expert is private), as uint32 [T, 4]."""
+    T, k = idx.shape
+    rec = np.zeros((T, 4), np.uint32)
+    offs = list(req_offset)
+    for t in range(T):
+        row = max(r for r in range(len(offs) - 1) if offs[r] <= t)
+        mask = sum(1 << j for j in range(k) if idx[t, j] >= n_pub)
+        pool = POOL_PUBLIC if mask == 0 else (POOL_PRIVATE if mask == (1 << k) - 1 else POOL_MIXED)
+        rec[t] = (layer | (int(allow[t]) << 16) | (pool << 24), row, t - offs[row], mask)
+    return rec
+
+
+def cache_tag_ok(cache: Optional[tuple], request: Optional[tuple]) -> bool:
+    """Cached state may serve a request only when both tags exist, both decisions are
+    well formed (0 or 1) and (decision, model revision, checkpoint fingerprint) are equal."""
+    if cache is None or request is None:
+        return False
+    if cache[0] not in (0, 1) or request[0] not in (0, 1):
+        return False
+    return tuple(cache) == tuple(request)

@@ -8,6 +8,8 @@ from ._native import (PMPE_BF16, PMPE_F32, PMPE_GATE_POOL_SOFTMAX, PMPE_GATE_REN
                       fingerprint_tensors, make_desc, pmpe_fingerprint,
                       pmpe_fingerprint_workspace_bytes, pmpe_backward,
                       pmpe_backward_workspace_bytes, pmpe_expert_ffn_train,
+                      PMPE_POOL_MIXED, PMPE_POOL_PRIVATE, PMPE_POOL_PUBLIC, CacheTag,
+                      make_cache_tag, pmpe_cache_tag_check, pmpe_route_record,
                       pmpe_audit, pmpe_check_desc, pmpe_combine, pmpe_dispatch, pmpe_expert_ffn,
                       pmpe_route, pmpe_version, pmpe_workspace_bytes)
 from .layer import AuditBuffers, GradBuffers, LayerBuffers, PolicyMaskedMoE  # noqa: F401

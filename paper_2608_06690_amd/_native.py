@@ -39,7 +39,12 @@ PMPE_DEV_PRIV_WEIGHTS_MISSING = 0x2
 STATUS_NAMES = {
     0: "PMPE_OK", -1: "PMPE_ERR_NULL", -2: "PMPE_ERR_SHAPE", -3: "PMPE_ERR_K_EXCEEDS_POOL",
     -4: "PMPE_ERR_DTYPE", -5: "PMPE_ERR_ALIGN", -6: "PMPE_ERR_WORKSPACE", -7: "PMPE_ERR_LAUNCH",
+    -8: "PMPE_ERR_TAG_MISMATCH",
 }
+PMPE_ERR_TAG_MISMATCH = -8
+PMPE_POOL_PUBLIC = 0
+PMPE_POOL_PRIVATE = 1
+PMPE_POOL_MIXED = 2
 
 
 class PmpeError(RuntimeError):
@@ -53,6 +58,23 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "hidden", "inter", "n_pub", "n_priv", "top_k", "n_shared", "shared_inter",
         "act_dtype", "w_dtype", "gate_mode", "route_mode")]
+
+
+class CacheTag(ctypes.Structure):
+    """pmpe_cache_tag: resolved decision (1 allow, 0 deny), model revision digest and
+    checkpoint fingerprint (32 bytes each)."""
+    _fields_ = [("decision", ctypes.c_uint32), ("model_revision", ctypes.c_uint8 * 32),
+                ("checkpoint_fingerprint", ctypes.c_uint8 * 32)]
+
+
+def make_cache_tag(decision: int, model_revision: bytes, checkpoint_fingerprint: bytes) -> CacheTag:
+    if len(model_revision) != 32 or len(checkpoint_fingerprint) != 32:
+        raise ValueError("model_revision and checkpoint_fingerprint are 32-byte digests")
+    t = CacheTag()
+    t.decision = decision
+    t.model_revision[:] = list(model_revision)
+    t.checkpoint_fingerprint[:] = list(checkpoint_fingerprint)
+    return t
 
 
 _P = ctypes.c_void_p
@@ -85,6 +107,10 @@ _lib.pmpe_backward.restype = _I32
 _lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 21 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn_train.restype = _I32
 _lib.pmpe_expert_ffn_train.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
+_lib.pmpe_route_record.restype = _I32
+_lib.pmpe_route_record.argtypes = [_DESC, _I32, _I32, _P, _P, _P, _I32, _P, _P]
+_lib.pmpe_cache_tag_check.restype = _I32
+_lib.pmpe_cache_tag_check.argtypes = [ctypes.POINTER(CacheTag), ctypes.POINTER(CacheTag)]
 _lib.pmpe_fingerprint_workspace_bytes.restype = _SZ
 _lib.pmpe_fingerprint_workspace_bytes.argtypes = [ctypes.c_uint64]
 _lib.pmpe_fingerprint.restype = _I32
@@ -93,7 +119,7 @@ _lib.pmpe_fingerprint.argtypes = [_P, ctypes.c_uint64, _P, _P, _SZ, _P]
 EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_check_desc",
             "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
             "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint", "pmpe_backward_workspace_bytes",
-            "pmpe_backward", "pmpe_expert_ffn_train"]
+            "pmpe_backward", "pmpe_expert_ffn_train", "pmpe_route_record", "pmpe_cache_tag_check"]
 
 PMPE_FP_LEAF_BYTES = 1024
 PMPE_FP_FANOUT = 16
@@ -239,3 +265,19 @@ def fingerprint_tensors(*tensors: torch.Tensor, stream=None) -> torch.Tensor:
     root = torch.empty(32, dtype=torch.uint8, device=dev)
     pmpe_fingerprint(digests, root, ws, stream=stream)
     return root
+
+
+def pmpe_route_record(desc, T, layer, topk_idx, allow, req_offset, R, rec, stream=None) -> None:
+    """rec: [T, 4] int32 device tensor (pmpe_route_rec per token)."""
+    _check(_lib.pmpe_route_record(ctypes.byref(desc), T, layer, _ptr(topk_idx), _ptr(allow),
+                                  _ptr(req_offset), R, _ptr(rec), _stream(stream)),
+           "pmpe_route_record")
+
+
+def pmpe_cache_tag_check(cache: Optional[CacheTag], request: Optional[CacheTag]) -> bool:
+    """True when the cached state may serve the request (every tag field equal)."""
+    st = _lib.pmpe_cache_tag_check(None if cache is None else ctypes.byref(cache),
+                                   None if request is None else ctypes.byref(request))
+    if st not in (PMPE_OK, PMPE_ERR_TAG_MISMATCH):
+        raise PmpeError(st, "pmpe_cache_tag_check")
+    return st == PMPE_OK

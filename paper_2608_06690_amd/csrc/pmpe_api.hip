@@ -162,6 +162,7 @@ const char* pmpe_status_string(int32_t status) {
     case PMPE_ERR_ALIGN: return "a pointer is not 16-byte aligned";
     case PMPE_ERR_WORKSPACE: return "workspace missing or too small";
     case PMPE_ERR_LAUNCH: return "the HIP runtime refused a kernel launch";
+    case PMPE_ERR_TAG_MISMATCH: return "cache tag does not match the request; reuse refused";
     default: return "unknown status";
   }
 }
@@ -269,6 +270,35 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
   AuditArgs a{T, R, audit_token_rows, allow, req_offset, req_private_rows, total_private_rows,
               deny_violations};
   return launched(launch_audit(a, (hipStream_t)stream));
+}
+
+static_assert(sizeof(pmpe_route_rec) == 16, "one record is one 16-byte store");
+static_assert(sizeof(pmpe_cache_tag) == 68, "cache tag layout");
+
+pmpe_status pmpe_route_record(const pmpe_layer_desc* d, int32_t T, int32_t layer,
+                              const int32_t* topk_idx, const uint8_t* allow,
+                              const int32_t* req_offset, int32_t R, pmpe_route_rec* rec,
+                              pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (layer < 0 || layer > 0xFFFF || R < 0 || R > PMPE_MAX_TOKENS) return PMPE_ERR_SHAPE;
+  if (T == 0) return PMPE_OK;
+  if (R < 1) return PMPE_ERR_SHAPE;
+  if (!topk_idx || !allow || !req_offset || !rec) return PMPE_ERR_NULL;
+  if (!aligned16(rec)) return PMPE_ERR_ALIGN;
+  RecordArgs a{T, R, d->top_k, d->n_pub, layer, topk_idx, allow, req_offset, (uint32_t*)rec};
+  return launched(launch_route_record(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_tag* request) {
+  if (!cache || !request) return PMPE_ERR_TAG_MISMATCH;
+  if (cache->decision > 1u || request->decision > 1u) return PMPE_ERR_TAG_MISMATCH;
+  unsigned diff = cache->decision ^ request->decision;
+  for (int i = 0; i < 32; ++i) {
+    diff |= (unsigned)(cache->model_revision[i] ^ request->model_revision[i]);
+    diff |= (unsigned)(cache->checkpoint_fingerprint[i] ^ request->checkpoint_fingerprint[i]);
+  }
+  return diff == 0 ? PMPE_OK : PMPE_ERR_TAG_MISMATCH;
 }
 
 size_t pmpe_backward_workspace_bytes(const pmpe_layer_desc* d, int32_t T) {

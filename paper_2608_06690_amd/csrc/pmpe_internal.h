@@ -153,6 +153,15 @@ struct AuditArgs {
 };
 hipError_t launch_audit(const AuditArgs& a, hipStream_t s);
 
+struct RecordArgs {
+  int T, R, k, n_pub, layer;
+  const int32_t* topk_idx;
+  const uint8_t* allow;
+  const int32_t* req_offset;
+  uint32_t* rec;  // [T, 4] words
+};
+hipError_t launch_route_record(const RecordArgs& a, hipStream_t s);
+
 struct BwdArgs {
   int T, H, I, k, n_pub, n_priv;
   const void* x;          // [T, H] bf16

@@ -141,6 +141,14 @@ class PolicyMaskedMoE:
         T = x.shape[0]
         N.pmpe_combine(self.desc, T, b.y_perm, b.token_row, b.topk_gate, b.y_shared, b.out, stream)
 
+    def route_record(self, T: int, b: LayerBuffers, req_offset, layer: int = 0,
+                     rec: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Route records of the last forward of this T: [T, 4] int32 (pmpe_route_rec)."""
+        rec = rec if rec is not None else torch.empty(T, 4, dtype=torch.int32, device=self.device)
+        N.pmpe_route_record(self.desc, T, layer, b.topk_idx, b.allow, req_offset,
+                            req_offset.numel() - 1, rec, stream)
+        return rec
+
     def audit(self, T: int, b: LayerBuffers, audit: AuditBuffers, req_offset, stream=None):
         R = req_offset.numel() - 1
         N.pmpe_audit(self.desc, T, audit.token_rows, b.allow, req_offset, R, audit.req_rows,

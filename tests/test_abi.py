@@ -180,7 +180,7 @@ def test_zero_tokens_launch_nothing():
 
 
 def test_status_strings():
-    for s in range(-7, 1):
+    for s in range(-8, 1):
         assert N.lib().pmpe_status_string(s).decode()
     assert P.pmpe_version() >= 10000
 
@@ -192,3 +192,32 @@ def test_policy_resolver_product_side():
         assert not P.resolve_policy(m)
     w = P.token_policy_words([{"allow_private": True}, None], [2, 1])
     assert [int(v) & 0xFFFFFFFF for v in w] == [N.PMPE_POLICY_ALLOW] * 2 + [0]
+
+
+def test_cache_tag_check_follows_the_oracle_rule():
+    """The library's host-side cache-tag guard against the oracle's rule on every single
+    field change, malformed decisions and missing tags."""
+    from oracle import pmpe_oracle as O
+    rev, fp = bytes(range(32)), bytes(range(100, 132))
+    cases = [((1, rev, fp), (1, rev, fp)), ((0, rev, fp), (0, rev, fp)), ((1, rev, fp), (0, rev, fp)),
+             ((2, rev, fp), (2, rev, fp)), ((0, rev, fp), (7, rev, fp))]
+    for i in range(32):
+        r2 = bytearray(rev); r2[i] ^= 0x40
+        f2 = bytearray(fp); f2[i] ^= 0x01
+        cases.append(((1, rev, fp), (1, bytes(r2), fp)))
+        cases.append(((0, rev, fp), (0, rev, bytes(f2))))
+    for c, r in cases:
+        got = P.pmpe_cache_tag_check(P.make_cache_tag(*c), P.make_cache_tag(*r))
+        assert got == O.cache_tag_ok(c, r), (c[0], r[0])
+    assert not P.pmpe_cache_tag_check(None, P.make_cache_tag(1, rev, fp))
+    assert not P.pmpe_cache_tag_check(P.make_cache_tag(1, rev, fp), None)
+
+
+def test_route_record_validation():
+    d = desc()
+    lib = N.lib()
+    assert lib.pmpe_route_record(ctypes.byref(d), 16, 70000, 0x1000, 0x2000, 0x3000, 1, 0x4000, None) == -2
+    assert lib.pmpe_route_record(ctypes.byref(d), 16, 0, 0x1000, 0x2000, 0x3000, 0, 0x4000, None) == -2
+    assert lib.pmpe_route_record(ctypes.byref(d), 16, 0, None, 0x2000, 0x3000, 1, 0x4000, None) == -1
+    assert lib.pmpe_route_record(ctypes.byref(d), 16, 0, 0x1000, 0x2000, 0x3000, 1, 0x4008, None) == -5
+    assert lib.pmpe_route_record(ctypes.byref(d), 0, 0, None, None, None, 0, None, None) == 0

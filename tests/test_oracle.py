@@ -662,3 +662,37 @@ def test_backward_k1_renorm_gate_is_constant():
     e = int(g.route.idx[t, 0]) - 6
     dX, _, _ = O.swiglu_backward(c["x"][t:t + 1], c["w13_priv"][e], c["w2_priv"][e], c["dout"][t:t + 1])
     assert np.allclose(g.dx[t], dX[0], rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# Route records and cache tags
+# ----------------------------------------------------------------------------
+
+def test_route_records_reconcile_with_execution_hooks():
+    """The records of the masked route say allow -> private-only, deny -> public-only,
+    and their private slots per request equal the rows the private experts' execution
+    hooks counted (the route log and the independent hooks agree)."""
+    cfg, L, x, req, words = tiny_case()
+    res = run_layer(cfg, L, x, words)
+    rec = O.route_records(res.route.idx, res.route.allow, req.offsets, cfg.n_pub, 7)
+    assert np.all(rec[:, 0] & 0xFFFF == 7)
+    decision = (rec[:, 0] >> 16) & 1
+    pool = rec[:, 0] >> 24
+    assert np.array_equal(decision, res.route.allow)
+    assert np.array_equal(pool, np.where(res.route.allow == 1, O.POOL_PRIVATE, O.POOL_PUBLIC))
+    pop = np.array([bin(int(m)).count("1") for m in rec[:, 3]])
+    per_req = [pop[a:b].sum() for a, b in zip(req.offsets[:-1], req.offsets[1:])]
+    assert per_req == [int(v) for v in O.audit(res.hook.rows, res.route.allow, req.offsets).req_private_rows]
+    # rows and positions enumerate every request
+    for r, (a, b) in enumerate(zip(req.offsets[:-1], req.offsets[1:])):
+        assert np.all(rec[a:b, 1] == r) and np.array_equal(rec[a:b, 2], np.arange(b - a))
+
+
+def test_cache_tag_rule():
+    fp, rev = bytes(range(32)), bytes(32)
+    assert O.cache_tag_ok((1, rev, fp), (1, rev, fp))
+    assert not O.cache_tag_ok((1, rev, fp), (0, rev, fp))          # across policies
+    assert not O.cache_tag_ok((0, rev, fp), (0, rev, fp[:31] + b"x"))
+    assert not O.cache_tag_ok((0, rev, fp), (0, b"\1" + rev[1:], fp))
+    assert not O.cache_tag_ok(None, (0, rev, fp))
+    assert not O.cache_tag_ok((2, rev, fp), (2, rev, fp))          # malformed decision
