@@ -564,3 +564,61 @@ def cache_tag_ok(cache: Optional[tuple], request: Optional[tuple]) -> bool:
     if cache[0] not in (0, 1) or request[0] not in (0, 1):
         return False
     return tuple(cache) == tuple(request)
+
+
+# ----------------------------------------------------------------------------
+# Request-gated LoRA control (Sec. 4.2 matched expert-LoRA baseline; Sec. 5.2 and
+# App. F.2: a request gate on an adapter is a logical switch, so the adapter can still
+# be physically executed for denied requests)
+# ----------------------------------------------------------------------------
+
+LORA_GATE_ROW, LORA_GATE_TILE, LORA_GATE_POSTHOC = 0, 1, 2
+LORA_TILE_ROWS = 64
+
+
+def lora_expert(X: np.ndarray, taus: np.ndarray, w13, w2, a13, b1, b3, a2, b2, scale: float):
+    """One public expert with rank-r adapters on its gate, up and down projections, the
+    adapter terms multiplied by the row's decision tau (1 allow, 0 deny):
+        g = X Wg^T + tau s (X Ag^T) Bg^T,  u = X Wu^T + tau s (X Au^T) Bu^T,
+        h = silu(g) u,  y = h Wd^T + tau s (h Ad^T) Bd^T
+    with a13 = [Ag; Au] ([2r, H]), b1 = Bg [I, r], b3 = Bu [I, r], a2 = Ad [r, I],
+    b2 = Bd [H, r]."""
+    X = np.asarray(X, np.float64)
+    t = np.asarray(taus, np.float64)[:, None]
+    w13 = np.asarray(w13, np.float64)
+    I = w13.shape[0] // 2
+    r = np.asarray(a13).shape[0] // 2
+    a13 = np.asarray(a13, np.float64)
+    G = X @ w13[:I].T + t * scale * ((X @ a13[:r].T) @ np.asarray(b1, np.float64).T)
+    U = X @ w13[I:].T + t * scale * ((X @ a13[r:].T) @ np.asarray(b3, np.float64).T)
+    Hh = G / (1.0 + np.exp(-G)) * U
+    return Hh @ np.asarray(w2, np.float64).T + t * scale * ((Hh @ np.asarray(a2, np.float64).T)
+                                                           @ np.asarray(b2, np.float64).T)
+
+
+def lora_physical_rows(idx: np.ndarray, taus: np.ndarray, n_experts: int, mode: int) -> np.ndarray:
+    """Adapter rows physically executed per token under each gate granularity. Rows are
+    the dispatch order (experts ascending, tokens ascending within an expert).
+    ROW      the gate is applied per row before any adapter work: allow rows only;
+    TILE     the gate is applied per tile of LORA_TILE_ROWS consecutive rows of one expert:
+             a tile runs its adapter when any of its rows allows, so denied rows that
+             share a tile with an allowed row are executed (and their result discarded);
+    POSTHOC  every row runs the adapter; the decision only scales the result."""
+    dp = dispatch(idx, n_experts)
+    T = idx.shape[0]
+    rows = np.zeros(T, np.int64)
+    for e in range(n_experts):
+        toks = dp.row_token[dp.offset[e]:dp.offset[e] + dp.count[e]]
+        for s in range(0, len(toks), LORA_TILE_ROWS):
+            tile = toks[s:s + LORA_TILE_ROWS]
+            for t in tile:
+                if mode == LORA_GATE_ROW:
+                    run = taus[t] == 1
+                elif mode == LORA_GATE_TILE:
+                    run = any(taus[u] == 1 for u in tile)
+                elif mode == LORA_GATE_POSTHOC:
+                    run = True
+                else:
+                    raise ValueError(mode)
+                rows[t] += int(run)
+    return rows

@@ -696,3 +696,58 @@ def test_cache_tag_rule():
     assert not O.cache_tag_ok((0, rev, fp), (0, b"\1" + rev[1:], fp))
     assert not O.cache_tag_ok(None, (0, rev, fp))
     assert not O.cache_tag_ok((2, rev, fp), (2, rev, fp))          # malformed decision
+
+
+# ----------------------------------------------------------------------------
+# Request-gated LoRA control
+# ----------------------------------------------------------------------------
+
+def _lora_case(seed=21, n=9, H=16, I=8, r=3):
+    rng = np.random.default_rng(seed)
+    f = lambda *s: rng.standard_normal(s) * 0.4  # noqa: E731
+    return (f(n, H), rng.integers(0, 2, n), f(2 * I, H), f(H, I), f(2 * r, H), f(I, r), f(I, r),
+            f(r, I), f(H, r))
+
+
+def test_lora_expert_allow_equals_merged_weights():
+    """For allowed rows the adapter equals a dense SwiGLU with merged weights
+    W + s B A; for denied rows it is the frozen expert."""
+    X, taus, w13, w2, a13, b1, b3, a2, b2 = _lora_case()
+    s = 2.0
+    r = a13.shape[0] // 2
+    I = w13.shape[0] // 2
+    got = O.lora_expert(X, taus, w13, w2, a13, b1, b3, a2, b2, s)
+    merged13 = np.concatenate([w13[:I] + s * b1 @ a13[:r], w13[I:] + s * b3 @ a13[r:]])
+    merged2 = w2 + s * b2 @ a2
+    xt = torch.tensor(X)
+    dense = lambda a, b: F.linear(F.silu(F.linear(xt, torch.tensor(a[:I]))) * F.linear(xt, torch.tensor(a[I:])), torch.tensor(b)).numpy()  # noqa: E731
+    ref_allow, ref_deny = dense(merged13, merged2), dense(w13, w2)
+    for i, t in enumerate(taus):
+        assert np.allclose(got[i], ref_allow[i] if t else ref_deny[i], rtol=1e-12, atol=1e-12)
+
+
+def test_lora_physical_rows_by_gate():
+    """Row gate: allowed rows only; post-hoc gate: every row; tile gate: in between, and
+    exactly the rows of tiles holding at least one allowed row."""
+    rng = np.random.default_rng(3)
+    T, k, E = 300, 2, 4
+    idx = np.sort(np.stack([rng.choice(E, k, replace=False) for _ in range(T)]), axis=1)
+    taus = (rng.random(T) < 0.3).astype(np.int64)
+    row = O.lora_physical_rows(idx, taus, E, O.LORA_GATE_ROW)
+    tile = O.lora_physical_rows(idx, taus, E, O.LORA_GATE_TILE)
+    post = O.lora_physical_rows(idx, taus, E, O.LORA_GATE_POSTHOC)
+    assert np.array_equal(row, k * taus) and np.array_equal(post, np.full(T, k))
+    assert np.all(row <= tile) and np.all(tile <= post)
+    assert tile[taus == 0].sum() > 0          # denied rows executed in mixed tiles
+    assert np.array_equal(tile[taus == 1], row[taus == 1])
+    # tile count by brute force over the dispatch order
+    dp = O.dispatch(idx, E)
+    brute = np.zeros(T, np.int64)
+    for e in range(E):
+        toks = list(dp.row_token[dp.offset[e]:dp.offset[e] + dp.count[e]])
+        for s in range(0, len(toks), 64):
+            blk = toks[s:s + 64]
+            if any(taus[t] for t in blk):
+                for t in blk:
+                    brute[t] += 1
+    assert np.array_equal(tile, brute)
