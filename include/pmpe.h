@@ -275,6 +275,51 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
                        uint32_t* deny_violations, pmpe_stream_t stream);
 
 /*
+ * pmpe_expert_ffn_lora - the request-gated LoRA control arm (Sec. 4.2 matched expert-LoRA
+ * baseline; Sec. 5.2 and App. F.2: a request gate on an adapter is a logical switch,
+ * and the paper's gated adapter still executed 1,225 times under deny). It exists to show
+ * that failure class next to the disjoint private pool; it is not a safe configuration.
+ *
+ * The frozen public experts run as in pmpe_expert_ffn, with rank-r adapters on each
+ * expert's gate, up and down projections scaled by s and by the row's decision tau
+ * (policy_word of its token == PMPE_POLICY_ALLOW):
+ *   g = Wg x + tau s Bg (Ag x),  u = Wu x + tau s Bu (Au x),  h = silu(g) u,
+ *   y = Wd h + tau s Bd (Ad h).
+ * gate selects where the decision is applied (PMPE_LORA_GATE_*): before any adapter work
+ * per row, per tile of PMPE_LORA_TILE_ROWS consecutive rows of one expert (a tile with
+ * an allowed row runs its adapters for all its rows), or only on the result. y_perm is
+ * the same under every gate; lora_rows[t] (uint32 [T], accumulated, not cleared) gains 2
+ * for every row of token t whose adapters physically ran (one for the gate/up adapters,
+ * one for the down adapter), so pmpe_audit over it reports denied tokens that executed
+ * adapters. Rows of private experts (none when the route used deny words only) get no
+ * adapter.
+ *
+ *   a13 [n_pub, 2r, H], b1 and b3 [n_pub, I, r], a2 [n_pub, r, I], b2 [n_pub, H, r] bf16
+ *   rank 1..128, scale the adapter scale s (alpha / r)
+ * Other arguments as pmpe_expert_ffn; ws: pmpe_expert_ffn_lora_workspace_bytes(d, T).
+ * Errors: as pmpe_expert_ffn, PMPE_ERR_DTYPE unless bf16, PMPE_ERR_SHAPE for a rank or gate
+ * out of range or hidden / inter above 8192.
+ */
+typedef enum {
+  PMPE_LORA_GATE_ROW = 0,     /* a denied row is skipped before any adapter work */
+  PMPE_LORA_GATE_TILE = 1,    /* the decision is taken per tile of rows */
+  PMPE_LORA_GATE_POSTHOC = 2  /* every row runs the adapters; the decision selects the result */
+} pmpe_lora_gate;
+#define PMPE_LORA_TILE_ROWS 64
+
+size_t pmpe_expert_ffn_lora_workspace_bytes(const pmpe_layer_desc* d, int32_t T);
+
+pmpe_status pmpe_expert_ffn_lora(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                                 const void* x, const int32_t* expert_count,
+                                 const int32_t* expert_offset, const int32_t* row_token,
+                                 const uint32_t* policy_word, const void* w13_pub,
+                                 const void* w2_pub, const void* a13, const void* b1,
+                                 const void* b3, const void* a2, const void* b2, int32_t rank,
+                                 float scale, int32_t gate, void* y_perm, uint32_t* lora_rows,
+                                 uint32_t* dev_status, void* ws, size_t ws_bytes,
+                                 pmpe_stream_t stream);
+
+/*
  * pmpe_route_record - export the route audit of one layer call: one record per token
  * with the layer, the request row, the token's position in the request, the selected
  * pool and the policy decision (App. B.1, fifth step of the fail-closed request

@@ -42,6 +42,10 @@ STATUS_NAMES = {
     -8: "PMPE_ERR_TAG_MISMATCH",
 }
 PMPE_ERR_TAG_MISMATCH = -8
+PMPE_LORA_GATE_ROW = 0
+PMPE_LORA_GATE_TILE = 1
+PMPE_LORA_GATE_POSTHOC = 2
+PMPE_LORA_TILE_ROWS = 64
 PMPE_POOL_PUBLIC = 0
 PMPE_POOL_PRIVATE = 1
 PMPE_POOL_MIXED = 2
@@ -107,6 +111,11 @@ _lib.pmpe_backward.restype = _I32
 _lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 21 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn_train.restype = _I32
 _lib.pmpe_expert_ffn_train.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
+_lib.pmpe_expert_ffn_lora_workspace_bytes.restype = _SZ
+_lib.pmpe_expert_ffn_lora_workspace_bytes.argtypes = [_DESC, _I32]
+_lib.pmpe_expert_ffn_lora.restype = _I32
+_lib.pmpe_expert_ffn_lora.argtypes = ([_DESC, _I32] + [_P] * 13 + [_I32, ctypes.c_float, _I32]
+                                      + [_P] * 3 + [_P, _SZ, _P])
 _lib.pmpe_route_record.restype = _I32
 _lib.pmpe_route_record.argtypes = [_DESC, _I32, _I32, _P, _P, _P, _I32, _P, _P]
 _lib.pmpe_cache_tag_check.restype = _I32
@@ -119,7 +128,8 @@ _lib.pmpe_fingerprint.argtypes = [_P, ctypes.c_uint64, _P, _P, _SZ, _P]
 EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_check_desc",
             "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
             "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint", "pmpe_backward_workspace_bytes",
-            "pmpe_backward", "pmpe_expert_ffn_train", "pmpe_route_record", "pmpe_cache_tag_check"]
+            "pmpe_backward", "pmpe_expert_ffn_train", "pmpe_route_record", "pmpe_cache_tag_check",
+            "pmpe_expert_ffn_lora_workspace_bytes", "pmpe_expert_ffn_lora"]
 
 PMPE_FP_LEAF_BYTES = 1024
 PMPE_FP_FANOUT = 16
@@ -281,3 +291,18 @@ def pmpe_cache_tag_check(cache: Optional[CacheTag], request: Optional[CacheTag])
     if st not in (PMPE_OK, PMPE_ERR_TAG_MISMATCH):
         raise PmpeError(st, "pmpe_cache_tag_check")
     return st == PMPE_OK
+
+
+def pmpe_expert_ffn_lora_workspace_bytes(desc: LayerDesc, T: int) -> int:
+    return int(_lib.pmpe_expert_ffn_lora_workspace_bytes(ctypes.byref(desc), T))
+
+
+def pmpe_expert_ffn_lora(desc, T, x_perm, x, expert_count, expert_offset, row_token, policy_word,
+                         w13_pub, w2_pub, a13, b1, b3, a2, b2, rank, scale, gate, y_perm,
+                         lora_rows, dev_status, ws, stream=None) -> None:
+    _check(_lib.pmpe_expert_ffn_lora(
+        ctypes.byref(desc), T, _ptr(x_perm), _ptr(x), _ptr(expert_count), _ptr(expert_offset),
+        _ptr(row_token), _ptr(policy_word), _ptr(w13_pub), _ptr(w2_pub), _ptr(a13), _ptr(b1),
+        _ptr(b3), _ptr(a2), _ptr(b2), rank, scale, gate, _ptr(y_perm), _ptr(lora_rows),
+        _ptr(dev_status), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+        _stream(stream)), "pmpe_expert_ffn_lora")

@@ -707,7 +707,10 @@ __global__ __launch_bounds__(THREADS) void gemm2_f32_kernel(FfnArgs a, int share
 
 }  // namespace
 
-hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) {
+hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) { return launch_expert_ffn_parts(a, s, 3); }
+
+// parts: bit 0 runs GEMM1 (x -> h), bit 1 runs GEMM2 (h -> y)
+hipError_t launch_expert_ffn_parts(const FfnArgs& a, hipStream_t s, int parts) {
   const int E = a.n_pub + a.n_priv;
   if (a.act_bf16) {
     // Average rows per routed expert picks the tile shape.
@@ -732,28 +735,34 @@ hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) {
     };
     if (large) {
       using C = CfgLarge;
-      if (a.ab_save)
+      if ((parts & 1) && a.ab_save)
         hipLaunchKernelGGL((gemm_bf16_kernel<C, true, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
-      else
+      else if (parts & 1)
         hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      if (parts & 2)
+        hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
     } else {
       using C = CfgSmall;
-      if (a.ab_save)
+      if ((parts & 1) && a.ab_save)
         hipLaunchKernelGGL((gemm_bf16_kernel<C, true, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
-      else
+      else if (parts & 1)
         hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BM, C::BN / 2, true, C::PER_CU), dim3(C::THREADS), 0, s, a);
-      hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
+      if (parts & 2)
+        hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BM, C::BN, false, C::PER_CU), dim3(C::THREADS), 0, s, a);
     }
   } else {
     const int m_slots = (a.T * a.k + F32_BM - 1) / F32_BM + E;
     const int sh_slots = (a.T + F32_BM - 1) / F32_BM;
-    hipLaunchKernelGGL(gemm1_f32_kernel, dim3((a.I + F32_NT - 1) / F32_NT, m_slots), dim3(THREADS), 0, s, a, 0);
-    if (a.Is > 0)
-      hipLaunchKernelGGL(gemm1_f32_kernel, dim3((a.Is + F32_NT - 1) / F32_NT, sh_slots), dim3(THREADS), 0, s, a, 1);
-    hipLaunchKernelGGL(gemm2_f32_kernel, dim3((a.H + F32_NT - 1) / F32_NT, m_slots), dim3(THREADS), 0, s, a, 0);
-    if (a.Is > 0)
-      hipLaunchKernelGGL(gemm2_f32_kernel, dim3((a.H + F32_NT - 1) / F32_NT, sh_slots), dim3(THREADS), 0, s, a, 1);
+    if (parts & 1) {
+      hipLaunchKernelGGL(gemm1_f32_kernel, dim3((a.I + F32_NT - 1) / F32_NT, m_slots), dim3(THREADS), 0, s, a, 0);
+      if (a.Is > 0)
+        hipLaunchKernelGGL(gemm1_f32_kernel, dim3((a.Is + F32_NT - 1) / F32_NT, sh_slots), dim3(THREADS), 0, s, a, 1);
+    }
+    if (parts & 2) {
+      hipLaunchKernelGGL(gemm2_f32_kernel, dim3((a.H + F32_NT - 1) / F32_NT, m_slots), dim3(THREADS), 0, s, a, 0);
+      if (a.Is > 0)
+        hipLaunchKernelGGL(gemm2_f32_kernel, dim3((a.H + F32_NT - 1) / F32_NT, sh_slots), dim3(THREADS), 0, s, a, 1);
+    }
   }
   return hipGetLastError();
 }

@@ -272,6 +272,56 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
   return launched(launch_audit(a, (hipStream_t)stream));
 }
 
+size_t pmpe_expert_ffn_lora_workspace_bytes(const pmpe_layer_desc* d, int32_t T) {
+  if (check_desc(d, T) != PMPE_OK) return 0;
+  return ffn_ws(d, T) + round_up((size_t)T * d->top_k * 2 * d->inter * 4);
+}
+
+pmpe_status pmpe_expert_ffn_lora(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                                 const void* x, const int32_t* expert_count,
+                                 const int32_t* expert_offset, const int32_t* row_token,
+                                 const uint32_t* policy_word, const void* w13_pub,
+                                 const void* w2_pub, const void* a13, const void* b1,
+                                 const void* b3, const void* a2, const void* b2, int32_t rank,
+                                 float scale, int32_t gate, void* y_perm, uint32_t* lora_rows,
+                                 uint32_t* dev_status, void* ws, size_t ws_bytes,
+                                 pmpe_stream_t stream) {
+  pmpe_status st = check_desc(d, T);
+  if (st != PMPE_OK) return st;
+  if (d->act_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
+  if (rank < 1 || rank > 128 || gate < PMPE_LORA_GATE_ROW || gate > PMPE_LORA_GATE_POSTHOC ||
+      d->hidden > 8192 || d->inter > 8192 || d->n_shared != 0)
+    return PMPE_ERR_SHAPE;
+  if (!expert_count || !expert_offset || !row_token || !w13_pub || !w2_pub || !y_perm ||
+      !a13 || !b1 || !b3 || !a2 || !b2 || !lora_rows)
+    return PMPE_ERR_NULL;
+  if (!x_perm && !x) return PMPE_ERR_NULL;
+  const void* al[] = {x_perm, x, w13_pub, w2_pub, a13, b1, b3, a2, b2, y_perm};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  const size_t fws = ffn_ws(d, T);
+  if (!ws || ws_bytes < fws + round_up((size_t)T * d->top_k * 2 * d->inter * 4)) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  float* ab = (float*)((char*)ws + fws);
+  // the adapters sit on the public experts; private rows (if any) run without weights
+  FfnArgs f{T, d->hidden, d->inter, d->n_pub, d->n_priv, d->top_k, 1, 0, x_perm, x, expert_count,
+            expert_offset, row_token, w13_pub, w2_pub, nullptr, nullptr, nullptr, nullptr, nullptr,
+            y_perm, lora_rows, nullptr, dev_status, ws, nullptr, ab};
+  // GEMM1 never touches the audit; GEMM2 only audits private rows, which run without
+  // weights here and are therefore neither executed nor counted
+  LoraArgs l{T, d->hidden, d->inter, d->top_k, d->n_pub, d->n_priv, rank, gate, scale,
+             expert_count, expert_offset, row_token, policy_word, x, x_perm,
+             (const uint16_t*)a13, (const uint16_t*)b1, (const uint16_t*)b3, (const uint16_t*)a2,
+             (const uint16_t*)b2, ab, (uint16_t*)ws, (uint16_t*)y_perm, lora_rows};
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = launch_expert_ffn_parts(f, s, 1);
+  if (e == hipSuccess) e = launch_lora_pre(l, s);
+  if (e == hipSuccess) e = launch_expert_ffn_parts(f, s, 2);
+  if (e == hipSuccess) e = launch_lora_post(l, s);
+  return launched(e);
+}
+
 static_assert(sizeof(pmpe_route_rec) == 16, "one record is one 16-byte store");
 static_assert(sizeof(pmpe_cache_tag) == 68, "cache tag layout");
 

@@ -131,6 +131,29 @@ struct FfnArgs {
   float* ab_save = nullptr;  // optional [T*k, 2I]: fp32 gate and up projections (bf16 path)
 };
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
+hipError_t launch_expert_ffn_parts(const FfnArgs& a, hipStream_t s, int parts);
+
+struct LoraArgs {
+  int T, H, I, k, n_pub, n_priv, rank, gate;
+  float scale;
+  const int32_t* count;
+  const int32_t* offset;
+  const int32_t* row_token;
+  const uint32_t* words;
+  const void* x;
+  const void* x_perm;
+  const uint16_t* a13;
+  const uint16_t* b1;
+  const uint16_t* b3;
+  const uint16_t* a2;
+  const uint16_t* b2;
+  const float* ab;     // [T*k, 2I] gate and up projections of the frozen expert
+  uint16_t* h;         // [T*k, I]
+  uint16_t* y_perm;    // [T*k, H]
+  uint32_t* lora_rows; // [T] adapter executions per token
+};
+hipError_t launch_lora_pre(const LoraArgs& a, hipStream_t s);
+hipError_t launch_lora_post(const LoraArgs& a, hipStream_t s);
 
 struct CombineArgs {
   int T, H, k, act_bf16;

@@ -141,6 +141,27 @@ class PolicyMaskedMoE:
         T = x.shape[0]
         N.pmpe_combine(self.desc, T, b.y_perm, b.token_row, b.topk_gate, b.y_shared, b.out, stream)
 
+    def forward_lora(self, x, words, lora, rank: int, scale: float, gate: int, audit: AuditBuffers,
+                     lora_rows: torch.Tensor, req_offset=None, stream=None) -> LayerBuffers:
+        """The request-gated LoRA control arm: every token routes in the public pool (deny
+        words), the adapters `lora` = (a13, b1, b3, a2, b2) on the public experts are
+        gated by the real `words`; lora_rows [T] int32 accumulates physical adapter rows."""
+        T = x.shape[0]
+        b = self.buffers(T)
+        deny = torch.zeros_like(words)
+        self.route(x, deny, b, stream)
+        self.dispatch(x, b, stream)
+        ws_bytes = N.pmpe_expert_ffn_lora_workspace_bytes(self.desc, T)
+        if b.ws.numel() < ws_bytes:
+            b.ws = torch.empty(ws_bytes, dtype=torch.uint8, device=self.device)
+        N.pmpe_expert_ffn_lora(self.desc, T, b.x_perm, x, b.expert_count, b.expert_offset,
+                               b.row_token, words, self.w13_pub, self.w2_pub, *lora, rank, scale,
+                               gate, b.y_perm, lora_rows, b.dev_status, b.ws, stream)
+        self.combine(x, b, stream)
+        if req_offset is not None:
+            self.audit(T, b, audit, req_offset, stream)
+        return b
+
     def route_record(self, T: int, b: LayerBuffers, req_offset, layer: int = 0,
                      rec: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
         """Route records of the last forward of this T: [T, 4] int32 (pmpe_route_rec)."""

@@ -205,6 +205,7 @@ def normal(key: int, shape: Sequence[int], std: float, dtype: torch.dtype = torc
 
 # tensor ids inside a layer's key space
 T_X, T_WR_PUB, T_WR_PRIV, T_BIAS, T_W13_PUB, T_W2_PUB, T_W13_PRIV, T_W2_PRIV, T_W13_SH, T_W2_SH, T_DOUT = range(11)
+T_LORA_A13, T_LORA_B1, T_LORA_B3, T_LORA_A2, T_LORA_B2 = range(11, 16)
 
 
 def torch_dtype(cfg: LayerConfig) -> torch.dtype:
@@ -243,6 +244,20 @@ def make_dout(cfg: LayerConfig, layer: int = 0, device="cpu", std: float = 1.0) 
     """Upstream gradient of the layer output, [T, H] in the activation dtype."""
     return normal(tensor_key(cfg.seed, layer, T_DOUT, 0), (cfg.tokens, cfg.hidden), std,
                   torch_dtype(cfg), device)
+
+
+def make_lora(cfg: LayerConfig, rank: int, layer: int = 0, device="cpu", std: float = 0.02):
+    """Rank-`rank` adapters on every public expert's gate, up and down projections (the
+    matched expert-LoRA control): a13 [n_pub, 2r, H] (gate rows then up rows), b1 and b3
+    [n_pub, I, r], a2 [n_pub, r, I], b2 [n_pub, H, r], in the activation dtype. Both
+    factors are drawn (not the zero-B initialisation), so the adapter is not a no-op."""
+    s, dt, n, H, I = cfg.seed, torch_dtype(cfg), cfg.n_pub, cfg.hidden, cfg.inter
+    k = lambda tid: tensor_key(s, layer, tid, rank)  # noqa: E731
+    return (normal(k(T_LORA_A13), (n, 2 * rank, H), std, dt, device),
+            normal(k(T_LORA_B1), (n, I, rank), std, dt, device),
+            normal(k(T_LORA_B3), (n, I, rank), std, dt, device),
+            normal(k(T_LORA_A2), (n, rank, I), std, dt, device),
+            normal(k(T_LORA_B2), (n, H, rank), std, dt, device))
 
 
 def make_router(cfg: LayerConfig, layer: int = 0, device="cpu"):
