@@ -622,3 +622,22 @@ def lora_physical_rows(idx: np.ndarray, taus: np.ndarray, n_experts: int, mode: 
                     raise ValueError(mode)
                 rows[t] += int(run)
     return rows
+
+
+# ----------------------------------------------------------------------------
+# Optimizer step over the private parameters (G2 of Sec. 2.2: only private parameters
+# are passed to the optimizer; Sec. 3.2 and App. C.1: fused AdamW)
+# ----------------------------------------------------------------------------
+
+def adamw_step(p: np.ndarray, g: np.ndarray, m: np.ndarray, v: np.ndarray, step: int, lr: float,
+               beta1: float, beta2: float, eps: float, weight_decay: float):
+    """AdamW (Loshchilov and Hutter, decoupled weight decay) in fp64: the parameter first
+    decays by lr * wd * p, then moves by lr * m_hat / (sqrt(v_hat) + eps) with the
+    bias-corrected moments of step `step` (1-based). Returns (p, m, v)."""
+    p = np.asarray(p, np.float64) * (1.0 - lr * weight_decay)
+    g = np.asarray(g, np.float64)
+    m = beta1 * np.asarray(m, np.float64) + (1.0 - beta1) * g
+    v = beta2 * np.asarray(v, np.float64) + (1.0 - beta2) * g * g
+    mh = m / (1.0 - beta1 ** step)
+    vh = v / (1.0 - beta2 ** step)
+    return p - lr * mh / (np.sqrt(vh) + eps), m, v

@@ -751,3 +751,26 @@ def test_lora_physical_rows_by_gate():
                 for t in blk:
                     brute[t] += 1
     assert np.array_equal(tile, brute)
+
+
+def test_adamw_step_equals_torch_adamw():
+    """Three steps of the oracle's AdamW against torch.optim.AdamW in fp64."""
+    rng = np.random.default_rng(8)
+    p0 = rng.standard_normal(37)
+    grads = [rng.standard_normal(37) for _ in range(3)]
+    hp = dict(lr=1e-2, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    tp = torch.tensor(p0, requires_grad=True)
+    opt = torch.optim.AdamW([tp], lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                            weight_decay=hp["weight_decay"])
+    p, m, v = p0.copy(), np.zeros(37), np.zeros(37)
+    for step, g in enumerate(grads, 1):
+        tp.grad = torch.tensor(g)
+        opt.step()
+        p, m, v = O.adamw_step(p, g, m, v, step, **hp)
+    assert np.allclose(p, tp.detach().numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_adamw_zero_gradient_only_decays():
+    p, m, v = O.adamw_step(np.array([2.0, -4.0]), np.zeros(2), np.zeros(2), np.zeros(2), 1,
+                           lr=0.1, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.5)
+    assert np.array_equal(p, np.array([2.0, -4.0]) * 0.95) and not m.any() and not v.any()
