@@ -294,6 +294,22 @@ def backward_bench(args, dev):
         torch.cuda.synchronize()
         times.append(e0.elapsed_time(e1) * 1e3)
     us = sum(times) / len(times)
+    # one AdamW step over the private parameters (fp32 router rows; bf16 experts with fp32
+    # master copies): read p, g, m, v and write p, m, v (+ the bf16 weight) per element
+    import paper_2608_06690_amd as P
+    opt = P.PrivateAdamW(layer, lr=1e-4)
+    opt.step(g)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        opt.step(g)
+    e1.record()
+    torch.cuda.synchronize()
+    opt_us = e0.elapsed_time(e1) * 1e3 / reps
+    n_f32 = layer.wr_priv.numel()
+    n_bf16 = layer.w13_priv.numel() + layer.w2_priv.numel()
+    opt_bytes = 28 * n_f32 + 30 * n_bf16
     counts = bufs.expert_count.cpu()
     R = cfg.tokens * cfg.top_k
     Rp = int(counts[cfg.n_pub:].sum())
@@ -310,8 +326,12 @@ def backward_bench(args, dev):
            "rows": R, "private_rows": Rp, "flop_algorithmic": alg, "flop_executed": executed,
            "tflops_algorithmic": alg / (us * 1e-6) / 1e12,
            "tflops_executed": executed / (us * 1e-6) / 1e12,
-           "frac_algorithmic": alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, "reps": reps}
-    del layer, x, bufs, g, dout
+           "frac_algorithmic": alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, "reps": reps,
+           "optimizer": {"kind": "AdamW over the private parameters only",
+                         "params": n_f32 + n_bf16, "us_per_step": opt_us, "bytes": opt_bytes,
+                         "hbm_gbs": opt_bytes / (opt_us * 1e-6) / 1e9,
+                         "hbm_frac": opt_bytes / (opt_us * 1e-6) / 1e9 / PEAK_HBM_GBS}}
+    del layer, x, bufs, g, dout, opt
     torch.cuda.empty_cache()
     return res
 

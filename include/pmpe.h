@@ -424,6 +424,26 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
                           pmpe_stream_t stream);
 
 /*
+ * pmpe_adamw - one AdamW step over one private parameter tensor (G2 of Sec. 2.2: the
+ * optimizer is given the private parameters only, so a frozen public tensor is never
+ * an argument of this call; Sec. 3.2 and App. C.1: fused AdamW). Decoupled weight decay:
+ *   p <- p (1 - lr wd); m <- b1 m + (1 - b1) g; v <- b2 v + (1 - b2) g^2;
+ *   p <- p - lr (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps)
+ * in fp32. A bf16 parameter (param_dtype PMPE_BF16) needs an fp32 master copy that takes
+ * the update; the bf16 weight is then its round-to-nearest-even value.
+ *
+ *   param     device, n elements of param_dtype (updated)
+ *   master    device fp32 [n] (updated) for PMPE_BF16, must be NULL for PMPE_F32
+ *   grad      device fp32 [n]; m, v device fp32 [n] (updated; zero before step 1)
+ *   step      1-based step count
+ * All pointers 16-byte aligned. Errors: PMPE_ERR_NULL, PMPE_ERR_ALIGN, PMPE_ERR_DTYPE,
+ * PMPE_ERR_SHAPE (step < 1, or a hyper-parameter that is not finite, or betas outside [0,1)).
+ */
+pmpe_status pmpe_adamw(void* param, int32_t param_dtype, float* master, const float* grad,
+                       float* m, float* v, uint64_t n, int32_t step, float lr, float beta1,
+                       float beta2, float eps, float weight_decay, pmpe_stream_t stream);
+
+/*
  * pmpe_fingerprint - SHA-256 tree digest of a device buffer, to show that the frozen
  * public weights are unchanged (hashed before and after training and after a reload,
  * Sec. 3.2 training and checkpointing, Sec. 5.1, App. C.1).

@@ -116,6 +116,8 @@ _lib.pmpe_expert_ffn_lora_workspace_bytes.argtypes = [_DESC, _I32]
 _lib.pmpe_expert_ffn_lora.restype = _I32
 _lib.pmpe_expert_ffn_lora.argtypes = ([_DESC, _I32] + [_P] * 13 + [_I32, ctypes.c_float, _I32]
                                       + [_P] * 3 + [_P, _SZ, _P])
+_lib.pmpe_adamw.restype = _I32
+_lib.pmpe_adamw.argtypes = [_P, _I32, _P, _P, _P, _P, ctypes.c_uint64, _I32] + [ctypes.c_float] * 5 + [_P]
 _lib.pmpe_route_record.restype = _I32
 _lib.pmpe_route_record.argtypes = [_DESC, _I32, _I32, _P, _P, _P, _I32, _P, _P]
 _lib.pmpe_cache_tag_check.restype = _I32
@@ -129,7 +131,7 @@ EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_
             "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
             "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint", "pmpe_backward_workspace_bytes",
             "pmpe_backward", "pmpe_expert_ffn_train", "pmpe_route_record", "pmpe_cache_tag_check",
-            "pmpe_expert_ffn_lora_workspace_bytes", "pmpe_expert_ffn_lora"]
+            "pmpe_expert_ffn_lora_workspace_bytes", "pmpe_expert_ffn_lora", "pmpe_adamw"]
 
 PMPE_FP_LEAF_BYTES = 1024
 PMPE_FP_FANOUT = 16
@@ -306,3 +308,13 @@ def pmpe_expert_ffn_lora(desc, T, x_perm, x, expert_count, expert_offset, row_to
         _ptr(b3), _ptr(a2), _ptr(b2), rank, scale, gate, _ptr(y_perm), _ptr(lora_rows),
         _ptr(dev_status), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
         _stream(stream)), "pmpe_expert_ffn_lora")
+
+
+def pmpe_adamw(param: torch.Tensor, master: Optional[torch.Tensor], grad: torch.Tensor,
+               m: torch.Tensor, v: torch.Tensor, step: int, lr: float, beta1: float, beta2: float,
+               eps: float, weight_decay: float, stream=None) -> None:
+    """One AdamW step of one parameter tensor (fp32, or bf16 with an fp32 master copy)."""
+    dt = PMPE_BF16 if param.dtype == torch.bfloat16 else PMPE_F32
+    _check(_lib.pmpe_adamw(_ptr(param), dt, _ptr(master), _ptr(grad), _ptr(m), _ptr(v),
+                           param.numel(), step, lr, beta1, beta2, eps, weight_decay,
+                           _stream(stream)), "pmpe_adamw")

@@ -1,5 +1,6 @@
 // C ABI of libpmpe: argument validation (host only, before any launch) and dispatch to
 // the kernel launchers. No exception crosses this boundary; nothing is allocated.
+#include <cmath>
 #include <new>
 
 #include "pmpe_internal.h"
@@ -386,6 +387,25 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
             (uint16_t*)(w + L.xp), (uint16_t*)(w + L.dy), (float*)(w + L.ab), (uint16_t*)(w + L.hh),
             (uint16_t*)(w + L.da), (float*)(w + L.dxr), (float*)(w + L.dz), (float*)(w + L.part)};
   return launched(launch_backward(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_adamw(void* param, int32_t param_dtype, float* master, const float* grad,
+                       float* m, float* v, uint64_t n, int32_t step, float lr, float beta1,
+                       float beta2, float eps, float weight_decay, pmpe_stream_t stream) {
+  if (param_dtype != PMPE_F32 && param_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
+  if ((param_dtype == PMPE_BF16) != (master != nullptr)) return PMPE_ERR_DTYPE;
+  if (step < 1 || !std::isfinite(lr) || !std::isfinite(eps) || !std::isfinite(weight_decay) ||
+      !(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f))
+    return PMPE_ERR_SHAPE;
+  if (n == 0) return PMPE_OK;
+  if (!param || !grad || !m || !v) return PMPE_ERR_NULL;
+  const void* al[] = {param, master, grad, m, v};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
+  const float c1 = (float)(1.0 - std::pow((double)beta1, (double)step));
+  const float c2 = (float)(1.0 - std::pow((double)beta2, (double)step));
+  AdamwArgs a{param, master, grad, m, v, n, lr, beta1, beta2, eps, 1.0f - lr * weight_decay, c1, c2};
+  return launched(launch_adamw(a, (hipStream_t)stream));
 }
 
 size_t pmpe_fingerprint_workspace_bytes(uint64_t nbytes) {

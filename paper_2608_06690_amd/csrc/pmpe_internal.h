@@ -176,6 +176,17 @@ struct AuditArgs {
 };
 hipError_t launch_audit(const AuditArgs& a, hipStream_t s);
 
+struct AdamwArgs {
+  void* param;          // fp32, or bf16 when master is given
+  float* master;        // fp32 master copy of a bf16 parameter, or NULL
+  const float* grad;
+  float* m;
+  float* v;
+  uint64_t n;
+  float lr, beta1, beta2, eps, decay, c1, c2;  // decay = 1 - lr wd; c = bias corrections
+};
+hipError_t launch_adamw(const AdamwArgs& a, hipStream_t s);
+
 struct RecordArgs {
   int T, R, k, n_pub, layer;
   const int32_t* topk_idx;

@@ -212,3 +212,26 @@ class PolicyMaskedMoE:
         if req_offset is not None:
             self.audit(x.shape[0], b, audit, req_offset, stream)
         return b
+
+
+class PrivateAdamW:
+    """AdamW over a layer's private parameters only: the private router rows (fp32) and
+    the private expert weights (bf16 with fp32 master copies). Public tensors are never
+    handed to the optimizer (they are not arguments of any call here)."""
+
+    def __init__(self, layer: PolicyMaskedMoE, lr: float = 1e-4, betas=(0.9, 0.999),
+                 eps: float = 1e-8, weight_decay: float = 0.0):
+        self.layer = layer
+        self.lr, self.betas, self.eps, self.wd = lr, betas, eps, weight_decay
+        self.params = [layer.wr_priv, layer.w13_priv, layer.w2_priv]
+        self.master = [None if p.dtype == torch.float32 else p.float() for p in self.params]
+        self.m = [torch.zeros(p.shape, dtype=torch.float32, device=p.device) for p in self.params]
+        self.v = [torch.zeros(p.shape, dtype=torch.float32, device=p.device) for p in self.params]
+        self.t = 0
+
+    def step(self, g: GradBuffers, stream=None) -> None:
+        self.t += 1
+        grads = [g.dwr_priv, g.dw13_priv, g.dw2_priv]
+        for p, mp, gr, m, v in zip(self.params, self.master, grads, self.m, self.v):
+            N.pmpe_adamw(p, mp, gr, m, v, self.t, self.lr, self.betas[0], self.betas[1], self.eps,
+                         self.wd, stream)

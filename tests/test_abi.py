@@ -221,3 +221,21 @@ def test_route_record_validation():
     assert lib.pmpe_route_record(ctypes.byref(d), 16, 0, None, 0x2000, 0x3000, 1, 0x4000, None) == -1
     assert lib.pmpe_route_record(ctypes.byref(d), 16, 0, 0x1000, 0x2000, 0x3000, 1, 0x4008, None) == -5
     assert lib.pmpe_route_record(ctypes.byref(d), 0, 0, None, None, None, 0, None, None) == 0
+
+
+def test_adamw_validation():
+    lib = N.lib()
+    a = (ctypes.c_float * 5)()
+    ok = dict(lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, wd=0.0)
+    call = lambda p, dt, master, n, step, b1=0.9, lr=1e-3: lib.pmpe_adamw(  # noqa: E731
+        p, dt, master, 0x2000, 0x3000, 0x4000, n, step, lr, b1, 0.999, 1e-8, 0.0, None)
+    assert call(0x1000, 2, None, 16, 1) == -4          # unknown dtype
+    assert call(0x1000, 1, None, 16, 1) == -4          # bf16 without master
+    assert call(0x1000, 0, 0x5000, 16, 1) == -4        # fp32 with master
+    assert call(0x1000, 0, None, 16, 0) == -2          # step < 1
+    assert call(0x1000, 0, None, 16, 1, b1=1.0) == -2  # beta out of range
+    assert call(0x1000, 0, None, 16, 1, lr=float("nan")) == -2
+    assert call(None, 0, None, 16, 1) == -1
+    assert call(0x1004, 0, None, 16, 1) == -5
+    assert call(None, 0, None, 0, 1) == 0              # nothing to do
+    del a, ok
