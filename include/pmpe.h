@@ -378,7 +378,10 @@ pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_t
  *
  *   dg_tj   = dout_t . y_{e_tj}(x_t)                     (y_perm of the forward)
  *   dz_tj   = g_tj (dg_tj - sum_i g_ti dg_ti)            (RENORM gates)
- *   dx_t    = sum_j [ W13_e^T (da; db)_tj + dz_tj W_r[e_tj] ]
+ *   dz_te   = p_te ([e selected] dg_te - sum_i p_ti dg_ti) (POOL_SOFTMAX, every pool
+ *             member e, p = softmax of the recomputed fp32 pool logits)
+ *   dx_t    = sum_j W13_e^T (da; db)_tj + sum_e dz_te W_r[e] (+ the shared experts'
+ *             input gradient for upstream dout_t)
  *   dW2_p   = sum over rows of private expert p of (g dout_t) h^T
  *   dW13_p  = sum over rows of p of (da; db) x_t^T
  *   dW_r[p] = sum over rows of p of dz x_t
@@ -387,15 +390,20 @@ pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_t
  * forward's. Every output element is summed by one thread in a fixed order: two calls
  * on the same inputs give bitwise equal results.
  *
- * Supported: bf16, PMPE_GATE_RENORM_TOPK, n_shared == 0, inter a multiple of 128;
- * either route mode (under PMPE_ROUTE_SOFT, deny rows that reached private experts
- * also feed private gradients - the control shows what the mask prevents).
+ * Supported: bf16, both gate modes (POOL_SOFTMAX with hidden <= 8192), shared experts
+ * (frozen), inter and n_shared * shared_inter multiples of 128; either route mode (under PMPE_ROUTE_SOFT,
+ * deny rows that reached private experts also feed private gradients - the control
+ * shows what the mask prevents).
  *
  *   x [T, H], dout [T, H]                       bf16
  *   topk_idx, topk_gate [T*k], expert_count, expert_offset [E], row_token, token_row
  *   [T*k], y_perm [T*k, H]                      the forward's route, dispatch and
  *                                               expert outputs
  *   wr_pub, wr_priv, w13_*, w2_*                the forward's weights
+ *   logit_bias [E] fp32 or NULL                 the route's logit bias (POOL_SOFTMAX
+ *                                               recomputes the pool logits; a token's
+ *                                               pool is the one its selection lies in)
+ *   w13_sh, w2_sh                               shared experts (n_shared > 0)
  *   ab [T*k, 2I] fp32 or NULL                   the gate and up projections saved by
  *                                               pmpe_expert_ffn_train; NULL recomputes
  *                                               them (one more grouped GEMM)
@@ -408,8 +416,8 @@ pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_t
  *   ws                                          pmpe_backward_workspace_bytes(d, T)
  *                                               bytes, 16-byte aligned
  *
- * Errors: PMPE_ERR_DTYPE (not bf16), PMPE_ERR_SHAPE (unsupported gate mode, shared
- * experts or inter), PMPE_ERR_NULL, PMPE_ERR_ALIGN, PMPE_ERR_WORKSPACE.
+ * Errors: PMPE_ERR_DTYPE (not bf16), PMPE_ERR_SHAPE (inter or the shared width not a
+ * multiple of 128), PMPE_ERR_NULL, PMPE_ERR_ALIGN, PMPE_ERR_WORKSPACE.
  */
 size_t pmpe_backward_workspace_bytes(const pmpe_layer_desc* d, int32_t T);
 
@@ -419,9 +427,10 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
                           const int32_t* row_token, const int32_t* token_row, const void* y_perm,
                           const float* wr_pub, const float* wr_priv, const void* w13_pub,
                           const void* w2_pub, const void* w13_priv, const void* w2_priv,
-                          const float* ab, float* dx, float* dw13_priv, float* dw2_priv,
-                          float* dwr_priv, uint32_t* grad_rows, void* ws, size_t ws_bytes,
-                          pmpe_stream_t stream);
+                          const float* logit_bias, const void* w13_sh, const void* w2_sh,
+                          const float* ab, float* dx, float* dw13_priv,
+                          float* dw2_priv, float* dwr_priv, uint32_t* grad_rows, void* ws,
+                          size_t ws_bytes, pmpe_stream_t stream);
 
 /*
  * pmpe_adamw - one AdamW step over one private parameter tensor (G2 of Sec. 2.2: the

@@ -108,7 +108,7 @@ _lib.pmpe_audit.argtypes = [_DESC, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]
 _lib.pmpe_backward_workspace_bytes.restype = _SZ
 _lib.pmpe_backward_workspace_bytes.argtypes = [_DESC, _I32]
 _lib.pmpe_backward.restype = _I32
-_lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 21 + [_P, _SZ, _P]
+_lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 24 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn_train.restype = _I32
 _lib.pmpe_expert_ffn_train.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn_lora_workspace_bytes.restype = _SZ
@@ -237,13 +237,14 @@ def pmpe_expert_ffn_train(desc, T, x_perm, x, expert_count, expert_offset, row_t
 
 
 def pmpe_backward(desc, T, x, dout, topk_idx, topk_gate, expert_count, expert_offset, row_token,
-                  token_row, y_perm, wr_pub, wr_priv, w13_pub, w2_pub, w13_priv, w2_priv, ab, dx,
-                  dw13_priv, dw2_priv, dwr_priv, grad_rows, ws, stream=None) -> None:
+                  token_row, y_perm, wr_pub, wr_priv, w13_pub, w2_pub, w13_priv, w2_priv,
+                  logit_bias, w13_sh, w2_sh, ab, dx, dw13_priv, dw2_priv, dwr_priv,
+                  grad_rows, ws, stream=None) -> None:
     _check(_lib.pmpe_backward(
         ctypes.byref(desc), T, _ptr(x), _ptr(dout), _ptr(topk_idx), _ptr(topk_gate),
         _ptr(expert_count), _ptr(expert_offset), _ptr(row_token), _ptr(token_row), _ptr(y_perm),
         _ptr(wr_pub), _ptr(wr_priv), _ptr(w13_pub), _ptr(w2_pub), _ptr(w13_priv), _ptr(w2_priv),
-        _ptr(ab), _ptr(dx), _ptr(dw13_priv), _ptr(dw2_priv), _ptr(dwr_priv), _ptr(grad_rows), _ptr(ws),
+        _ptr(logit_bias), _ptr(w13_sh), _ptr(w2_sh), _ptr(ab), _ptr(dx), _ptr(dw13_priv), _ptr(dw2_priv), _ptr(dwr_priv), _ptr(grad_rows), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)), "pmpe_backward")
 
 

@@ -94,7 +94,9 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
       g[j] = a.topk_gate[t * k + j];
       sum += g[j] * v;
     }
-    for (int j = 0; j < k; ++j) s_dz[j] = g[j] * (dg[j] - sum);
+    // RENORM: the logit gradient lives on the k selected experts; POOL_SOFTMAX keeps
+    // dg (per slot) for the pool pass, which needs every pool logit
+    for (int j = 0; j < k; ++j) s_dz[j] = a.pool_gates ? dg[j] : g[j] * (dg[j] - sum);
   }
   __syncthreads();
   if (tid < k) a.dz_row[s_row[tid]] = s_dz[tid];
@@ -144,7 +146,8 @@ struct GemmArgs {
   const int32_t* offset;
   int g_begin, g_end, n_pub;
   int M, N, K;
-  // EPI_SWIGLU_BWD: [a; b] rows (fp32, 2I per row) in, [da; db] and h (bf16) out
+  int fixed_rows;          // ROWS: > 0 means one group of this many rows at row 0, weights B
+  // EPI_SWIGLU_BWD: [a; b] rows (fp32, 2I per row) in, [da; db] and h (bf16, if Hh) out
   const float* AB;
   uint16_t* dA13;
   uint16_t* Hh;
@@ -182,6 +185,15 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
     Kg = p.count[g];
     base = p.offset[g];
     rows = TM;
+  } else if (p.fixed_rows > 0) {
+    const int mt = (p.fixed_rows + TM - 1) / TM;
+    if (L >= mt * ntn) return;
+    g = 0;
+    n0 = (L / mt) * TN;
+    m0 = (L % mt) * TM;
+    rows = min(TM, p.fixed_rows - m0);
+    base = m0;
+    Kg = p.K;
   } else {
     if (tid < 64) {
       int running = 0;
@@ -212,7 +224,7 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
     Kg = p.K;
   }
   const uint16_t* Bg = p.B;
-  if (!KROWS) Bg = (g < p.n_pub) ? p.B + (size_t)g * p.strideB : p.B_priv + (size_t)(g - p.n_pub) * p.strideB;
+  if (!KROWS && p.fixed_rows == 0) Bg = (g < p.n_pub) ? p.B + (size_t)g * p.strideB : p.B_priv + (size_t)(g - p.n_pub) * p.strideB;
 
   u32x4 ra[4], rb[4];
   // Registers of K step k0: direct operands 4 x 16 bytes of rows (t + 256 i) / 8,
@@ -334,7 +346,7 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
           const float db = v * ga * s;
           p.dA13[r * 2 * p.I + n] = (uint16_t)f32_to_bf16_rne(da);
           p.dA13[r * 2 * p.I + p.I + n] = (uint16_t)f32_to_bf16_rne(db);
-          p.Hh[r * p.I + n] = (uint16_t)f32_to_bf16_rne(ga * s * ub);
+          if (p.Hh) p.Hh[r * p.I + n] = (uint16_t)f32_to_bf16_rne(ga * s * ub);
         }
       }
     }
@@ -343,7 +355,63 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
 // ---------------------------------------------------------------------------
 // Reductions
 // ---------------------------------------------------------------------------
-// dx_t = sum_j (dXr[r_j] + dz_j W_r[e_j]) in slot order, four columns per thread.
+// Softmax over the whole permitted pool (POOL_SOFTMAX), block t: the pool logits
+// z_e = x_t . W_r[e] (+ b_e) are recomputed in fp32 (one wave per logit, fixed-order
+// reduction), p = softmax(z), and dz_e = p_e ([e selected] dg_e - sum_sel p_i dg_i) for
+// every pool member e, written to dz_pool[t, e - first id of the pool].
+__global__ __launch_bounds__(BT) void bwd_pool_dz_kernel(BwdArgs a) {
+  extern __shared__ float s_dyn[];
+  float* s_x = s_dyn;               // [H]
+  float* s_z = s_dyn + a.H;         // [pool]
+  __shared__ float s_red[2];
+  const int t = blockIdx.x, H = a.H, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the pool of the token is the one its selection lies in (a masked route never mixes
+  // pools; the soft control ranks the concatenated pool)
+  const bool priv = a.topk_idx[t * a.k] >= a.n_pub;
+  const int first = a.soft ? 0 : (priv ? a.n_pub : 0);
+  const int pool = a.soft ? a.n_pub + a.n_priv : (priv ? a.n_priv : a.n_pub);
+  const uint16_t* xt = (const uint16_t*)a.x + (size_t)t * H;
+  for (int h = tid; h < H; h += BT) s_x[h] = bf16_to_f32(xt[h]);
+  __syncthreads();
+  for (int i = wave; i < pool; i += BT / 64) {
+    const int e = first + i;
+    const float* w = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
+    float s = 0.f;
+    for (int h = lane; h < H; h += 64) s += s_x[h] * w[h];
+    s = wave_sum(s);
+    if (lane == 0) s_z[i] = a.bias ? s + a.bias[e] : s;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float mx = -INFINITY;
+    for (int i = 0; i < pool; ++i) mx = fmaxf(mx, s_z[i]);
+    float den = 0.f;
+    for (int i = 0; i < pool; ++i) den += __expf(s_z[i] - mx);
+    // sum over the selection of p_i dg_i (dg per slot from the row pass)
+    float sel = 0.f;
+    for (int j = 0; j < a.k; ++j) {
+      const int e = a.topk_idx[t * a.k + j];
+      sel += __expf(s_z[e - first] - mx) / den * a.dz_row[a.token_row[t * a.k + j]];
+    }
+    s_red[0] = mx;
+    s_red[1] = den;
+    s_z[pool] = sel;  // scratch slot after the pool
+  }
+  __syncthreads();
+  const float mx = s_red[0], den = s_red[1], sel = s_z[pool];
+  float* dzp = a.dz_pool + (size_t)t * a.pool_stride;
+  for (int i = tid; i < pool; i += BT) {
+    const float pe = __expf(s_z[i] - mx) / den;
+    float u = 0.f;
+    for (int j = 0; j < a.k; ++j)
+      if (a.topk_idx[t * a.k + j] == first + i) u = a.dz_row[a.token_row[t * a.k + j]];
+    dzp[i] = pe * (u - sel);
+  }
+}
+
+// dx_t = sum_j dXr[r_j] (slot order) + router term + shared-expert term, four columns per
+// thread. Router term: RENORM sum_j dz_j W_r[e_j]; POOL_SOFTMAX sum over the pool of
+// dz_e W_r[e] in id order.
 __global__ __launch_bounds__(BT) void bwd_dx_kernel(BwdArgs a) {
   __shared__ int s_r[PMPE_MAX_TOPK];
   __shared__ const float* s_w[PMPE_MAX_TOPK];
@@ -352,10 +420,14 @@ __global__ __launch_bounds__(BT) void bwd_dx_kernel(BwdArgs a) {
   if (tid < k) {
     const int r = a.token_row[t * k + tid], e = a.topk_idx[t * k + tid];
     s_r[tid] = r;
-    s_dz[tid] = a.dz_row[r];
+    s_dz[tid] = a.pool_gates ? 0.f : a.dz_row[r];
     s_w[tid] = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
   }
   __syncthreads();
+  const bool priv = a.topk_idx[t * k] >= a.n_pub;
+  const int first = a.soft ? 0 : (priv ? a.n_pub : 0);
+  const int pool = a.soft ? a.n_pub + a.n_priv : (priv ? a.n_priv : a.n_pub);
+  const float* dzp = a.pool_gates ? a.dz_pool + (size_t)t * a.pool_stride : nullptr;
   for (int h = tid * 4; h < H; h += BT * 4) {
     f32x4 s = {0, 0, 0, 0};
     for (int j = 0; j < k; ++j) {
@@ -363,7 +435,43 @@ __global__ __launch_bounds__(BT) void bwd_dx_kernel(BwdArgs a) {
       const f32x4 w = *(const f32x4*)(s_w[j] + h);
       s += d + s_dz[j] * w;
     }
+    if (dzp) {
+      for (int i = 0; i < pool; ++i) {
+        const int e = first + i;
+        const float* w = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
+        s += dzp[i] * *(const f32x4*)(w + h);
+      }
+    }
+    if (a.dXsh) s += *(const f32x4*)(a.dXsh + (size_t)t * H + h);
     *(f32x4*)(a.dx + (size_t)t * H + h) = s;
+  }
+}
+
+// POOL_SOFTMAX router-row gradient of private expert p: every token whose pool holds p
+// contributes dz x_t (the gradient is dense over the pool). Block (p, c) sums a fixed
+// chunk of tokens in ascending order, eight columns per thread.
+__global__ __launch_bounds__(BT) void bwd_dwr_pool_part_kernel(BwdArgs a) {
+  const int pe = blockIdx.x, c = blockIdx.y, H = a.H, T = a.T;
+  if (c == 0 && threadIdx.x == 0 && a.grad_rows) a.grad_rows[pe] = (uint32_t)a.count[a.n_pub + pe];
+  const int per = (T + BWD_DWR_SPLIT - 1) / BWD_DWR_SPLIT;
+  const int t0 = min(T, c * per), t1 = min(T, (c + 1) * per);
+  float* part = a.dwr_part + ((size_t)pe * BWD_DWR_SPLIT + c) * H;
+  const uint16_t* x = (const uint16_t*)a.x;
+  for (int h = threadIdx.x * 8; h < H; h += BT * 8) {
+    float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int t = t0; t < t1; ++t) {
+      if (!a.soft && a.topk_idx[t * a.k] < a.n_pub) continue;  // a public-pool token
+      const int idx = a.soft ? a.n_pub + pe : pe;
+      const float dz = a.dz_pool[(size_t)t * a.pool_stride + idx];
+      const u32x4 v = *(const u32x4*)(x + (size_t)t * H + h);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        s[2 * q] += dz * bf16_to_f32(v[q] & 0xFFFFu);
+        s[2 * q + 1] += dz * bf16_to_f32(v[q] >> 16);
+      }
+    }
+    *(f32x4*)(part + h) = f32x4{s[0], s[1], s[2], s[3]};
+    *(f32x4*)(part + h + 4) = f32x4{s[4], s[5], s[6], s[7]};
   }
 }
 
@@ -417,6 +525,34 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
   bwd_rows_kernel<<<a.T, BT, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (a.pool_gates) {
+    const size_t lds = ((size_t)H + a.pool_stride + 1) * sizeof(float);
+    bwd_pool_dz_kernel<<<a.T, BT, lds, s>>>(a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.Is > 0) {
+    // shared experts: one group of all T tokens, gate 1, frozen weights (input gradient only)
+    GemmArgs sh{};
+    sh.fixed_rows = a.T;
+    sh.A = (const uint16_t*)a.x; sh.lda = H;
+    sh.B = (const uint16_t*)a.w13_sh; sh.ldb = H;
+    sh.C = a.AB_sh; sh.ldc = 2 * a.Is; sh.N = 2 * a.Is; sh.K = H;
+    const int mt = (a.T + TM - 1) / TM;
+    e = launch_gemm<false, false, false, EPI_F32>(sh, mt * (sh.N / TN), s);
+    if (e != hipSuccess) return e;
+    sh.A = (const uint16_t*)a.dout; sh.lda = H;
+    sh.B = (const uint16_t*)a.w2_sh; sh.ldb = a.Is;
+    sh.C = nullptr; sh.N = a.Is; sh.K = H;
+    sh.AB = a.AB_sh; sh.dA13 = a.dA13_sh; sh.Hh = nullptr; sh.I = a.Is;
+    e = launch_gemm<false, true, false, EPI_SWIGLU_BWD>(sh, mt * (sh.N / TN), s);
+    if (e != hipSuccess) return e;
+    sh.A = a.dA13_sh; sh.lda = 2 * a.Is;
+    sh.B = (const uint16_t*)a.w13_sh; sh.ldb = H;
+    sh.C = a.dXsh; sh.ldc = H; sh.N = H; sh.K = 2 * a.Is;
+    e = launch_gemm<false, true, false, EPI_F32>(sh, mt * (sh.N / TN), s);
+    if (e != hipSuccess) return e;
+  }
   // ROWS launches: at most R / TM + E row tiles over all groups
   const int mt_max = R / TM + E;
   GemmArgs g{};
@@ -467,7 +603,10 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     w.C = a.dw13_priv; w.ldc = H; w.strideC = (size_t)2 * I * H; w.M = 2 * I; w.N = H;
     e = launch_gemm<true, true, true, EPI_F32>(w, a.n_priv * (2 * I / TM) * (H / TN), s);
     if (e != hipSuccess) return e;
-    bwd_dwr_part_kernel<<<dim3(a.n_priv, BWD_DWR_SPLIT), BT, 0, s>>>(a);
+    if (a.pool_gates)
+      bwd_dwr_pool_part_kernel<<<dim3(a.n_priv, BWD_DWR_SPLIT), BT, 0, s>>>(a);
+    else
+      bwd_dwr_part_kernel<<<dim3(a.n_priv, BWD_DWR_SPLIT), BT, 0, s>>>(a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     bwd_dwr_sum_kernel<<<dim3((H + BT - 1) / BT, a.n_priv), BT, 0, s>>>(a);

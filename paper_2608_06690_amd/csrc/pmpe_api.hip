@@ -75,8 +75,12 @@ pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR
 
 // backward workspace: Xp, dY, [a; b], h, [da; db], row input gradients, row dz
 struct BwdLayout {
-  size_t xp, dy, ab, hh, da, dxr, dz, part, total;
+  size_t xp, dy, ab, hh, da, dxr, dz, part, dzp, absh, dash, dxsh, total;
 };
+int bwd_pool_stride(const pmpe_layer_desc* d) {
+  if (d->route_mode == PMPE_ROUTE_SOFT) return d->n_pub + d->n_priv;
+  return d->n_pub > d->n_priv ? d->n_pub : d->n_priv;
+}
 BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
   const size_t R = (size_t)T * d->top_k, H = d->hidden, I = d->inter;
   BwdLayout L;
@@ -89,6 +93,11 @@ BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
   L.dxr = o; o += round_up(R * H * 4);
   L.dz = o; o += round_up(R * 4);
   L.part = o; o += round_up((size_t)d->n_priv * BWD_DWR_SPLIT * H * 4);
+  const size_t Tt = (size_t)T, Is = (size_t)d->n_shared * d->shared_inter;
+  L.dzp = o; o += d->gate_mode == PMPE_GATE_POOL_SOFTMAX ? round_up(Tt * bwd_pool_stride(d) * 4) : 0;
+  L.absh = o; o += round_up(Tt * 2 * Is * 4);
+  L.dash = o; o += round_up(Tt * 2 * Is * 2);
+  L.dxsh = o; o += Is > 0 ? round_up(Tt * H * 4) : 0;
   L.total = o;
   return L;
 }
@@ -97,8 +106,10 @@ pmpe_status check_backward_desc(const pmpe_layer_desc* d, int32_t T) {
   pmpe_status st = check_desc(d, T);
   if (st != PMPE_OK) return st;
   if (d->act_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
-  if (d->gate_mode != PMPE_GATE_RENORM_TOPK || d->n_shared != 0 || d->inter % 128 != 0)
-    return PMPE_ERR_SHAPE;
+  if (d->inter % 128 != 0) return PMPE_ERR_SHAPE;
+  if (d->n_shared > 0 && ((int64_t)d->n_shared * d->shared_inter) % 128 != 0) return PMPE_ERR_SHAPE;
+  // the pool-softmax pass stages one x row in fp32 LDS
+  if (d->gate_mode == PMPE_GATE_POOL_SOFTMAX && d->hidden > 8192) return PMPE_ERR_SHAPE;
   return PMPE_OK;
 }
 
@@ -363,9 +374,10 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
                           const int32_t* row_token, const int32_t* token_row, const void* y_perm,
                           const float* wr_pub, const float* wr_priv, const void* w13_pub,
                           const void* w2_pub, const void* w13_priv, const void* w2_priv,
-                          const float* ab, float* dx, float* dw13_priv, float* dw2_priv,
-                          float* dwr_priv, uint32_t* grad_rows, void* ws, size_t ws_bytes,
-                          pmpe_stream_t stream) {
+                          const float* logit_bias, const void* w13_sh, const void* w2_sh,
+                          const float* ab, float* dx, float* dw13_priv,
+                          float* dw2_priv, float* dwr_priv, uint32_t* grad_rows, void* ws,
+                          size_t ws_bytes, pmpe_stream_t stream) {
   pmpe_status st = check_backward_desc(d, T);
   if (st != PMPE_OK) return st;
   if (!x || !dout || !topk_idx || !topk_gate || !expert_count || !expert_offset || !row_token ||
@@ -373,7 +385,8 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
     return PMPE_ERR_NULL;
   if (d->n_priv > 0 && (!wr_priv || !w13_priv || !w2_priv || !dw13_priv || !dw2_priv || !dwr_priv))
     return PMPE_ERR_NULL;
-  const void* al[] = {x, dout, y_perm, w13_pub, w2_pub, w13_priv, w2_priv, ab};
+  if (d->n_shared > 0 && (!w13_sh || !w2_sh)) return PMPE_ERR_NULL;
+  const void* al[] = {x, dout, y_perm, w13_pub, w2_pub, w13_priv, w2_priv, ab, w13_sh, w2_sh};
   for (const void* p : al)
     if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
   if (T == 0) return PMPE_OK;
@@ -385,7 +398,12 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
             expert_count, expert_offset, row_token, token_row, y_perm, wr_pub, wr_priv, w13_pub,
             w2_pub, w13_priv, w2_priv, ab, dx, dw13_priv, dw2_priv, dwr_priv, grad_rows,
             (uint16_t*)(w + L.xp), (uint16_t*)(w + L.dy), (float*)(w + L.ab), (uint16_t*)(w + L.hh),
-            (uint16_t*)(w + L.da), (float*)(w + L.dxr), (float*)(w + L.dz), (float*)(w + L.part)};
+            (uint16_t*)(w + L.da), (float*)(w + L.dxr), (float*)(w + L.dz), (float*)(w + L.part),
+            d->gate_mode == PMPE_GATE_POOL_SOFTMAX ? 1 : 0, d->route_mode == PMPE_ROUTE_SOFT ? 1 : 0,
+            bwd_pool_stride(d), logit_bias, (float*)(w + L.dzp),
+            d->n_shared > 0 ? d->n_shared * d->shared_inter : 0, w13_sh, w2_sh,
+            (float*)(w + L.absh), (uint16_t*)(w + L.dash),
+            d->n_shared > 0 ? (float*)(w + L.dxsh) : nullptr};
   return launched(launch_backward(a, (hipStream_t)stream));
 }
 

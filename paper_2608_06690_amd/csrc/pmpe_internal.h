@@ -226,8 +226,19 @@ struct BwdArgs {
   uint16_t* Hh;    // [T*k, I]
   uint16_t* dA13;  // [T*k, 2I]
   float* dXr;      // [T*k, H]
-  float* dz_row;   // [T*k]
+  float* dz_row;   // [T*k]: RENORM logit gradient per row; POOL_SOFTMAX gate gradient
   float* dwr_part; // [n_priv, BWD_DWR_SPLIT, H]
+  // softmax over the whole pool and the soft-routing control
+  int pool_gates, soft, pool_stride;
+  const float* bias;      // [E] or NULL
+  float* dz_pool;         // [T, pool_stride]
+  // shared experts (frozen; input gradient only)
+  int Is;
+  const void* w13_sh;     // [2 Is, H]
+  const void* w2_sh;      // [H, Is]
+  float* AB_sh;           // [T, 2 Is]
+  uint16_t* dA13_sh;      // [T, 2 Is]
+  float* dXsh;            // [T, H] or NULL
 };
 constexpr int BWD_DWR_SPLIT = 16;  // row chunks per private expert in the router-row gradient
 

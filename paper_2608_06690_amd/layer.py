@@ -197,6 +197,7 @@ class PolicyMaskedMoE:
         N.pmpe_backward(self.desc, T, x, dout, b.topk_idx, b.topk_gate, b.expert_count,
                         b.expert_offset, b.row_token, b.token_row, b.y_perm, self.wr_pub,
                         self.wr_priv, self.w13_pub, self.w2_pub, self.w13_priv, self.w2_priv,
+                        self.bias, self.w13_sh, self.w2_sh,
                         b.ab if use_saved else None, g.dx, g.dw13_priv, g.dw2_priv, g.dwr_priv, g.grad_rows, g.ws, stream)
         return g
 

@@ -127,6 +127,72 @@ def test_training_forward_output_equals_inference_forward():
     assert torch.isfinite(h).all()
 
 
+DS_SMALL = dict(tokens=400, requests=4, hidden=256, inter=128, n_pub=16, n_priv=8, top_k=4,
+                n_shared=2, shared_inter=128)
+
+
+@pytest.mark.parametrize("soft", [False, True], ids=["masked", "soft"])
+def test_backward_pool_softmax_and_shared_experts(soft):
+    """DeepSeek-shaped layer: softmax over the whole pool (the router gradient is dense
+    over the pool), a logit bias, and two always-on shared experts (frozen, input gradient
+    only)."""
+    cfg = W.scaled_config(W.get_config("deepseek"), **DS_SMALL)
+    log(f"backward deepseek-shaped {DS_SMALL} soft={soft}")
+    oi = C.oracle_inputs(cfg)
+    req = W.make_requests(cfg)
+    words = O.compile_words(req.metas, req.lengths)
+    rt, dout = oracle_route_and_dout(cfg, oi, words, soft)
+    layer, Lw, b, g, _, _ = forward_backward(cfg, soft, dout)
+    idx = b.topk_idx.view(cfg.tokens, cfg.top_k).cpu().numpy()
+    keep = ~rt.near_tie
+    assert np.array_equal(idx[keep], rt.idx[keep])
+    ref = O.layer_backward(oi.x, oi.wr_pub, oi.wr_priv, oi.bias, stacked(oi.w13_pub, cfg.n_pub),
+                           stacked(oi.w2_pub, cfg.n_pub), stacked(oi.w13_priv, cfg.n_priv),
+                           stacked(oi.w2_priv, cfg.n_priv), words, cfg.top_k, C.np64(dout),
+                           cfg.gate_mode, oi.w13_sh, oi.w2_sh, soft=soft)
+    errs = {
+        "dx": C.rel_l2(g.dx.cpu().numpy(), ref.dx),
+        "dw13": C.rel_l2(g.dw13_priv.cpu().numpy(), ref.dw13_priv),
+        "dw2": C.rel_l2(g.dw2_priv.cpu().numpy(), ref.dw2_priv),
+        "dwr": C.rel_l2(g.dwr_priv.cpu().numpy(), ref.dwr_priv),
+    }
+    log(f"  rel_l2 {errs}")
+    for k_, v in errs.items():
+        assert v <= RTOL, (k_, v)
+    # with pool gates every allowed token trains every private router row
+    if not soft:
+        assert np.all(np.abs(g.dwr_priv.cpu().numpy()).sum(axis=1) > 0)
+
+
+def test_backward_deepseek_full_size_sampled_experts():
+    """DeepSeek-shaped layer at full size (8192 tokens, 2 shared + 64 + 16 experts, top-6,
+    pool softmax, bias): the weight gradients of two private experts against the oracle's
+    SwiGLU backward on their rows."""
+    cfg = W.get_config("deepseek")
+    log("backward deepseek full size")
+    oi = C.oracle_inputs(cfg)
+    req = W.make_requests(cfg)
+    words = O.compile_words(req.metas, req.lengths)
+    rt, dout = oracle_route_and_dout(cfg, oi, words)
+    layer, Lw, b, g, _, _ = forward_backward(cfg, False, dout)
+    idx = b.topk_idx.view(cfg.tokens, cfg.top_k).cpu().numpy()
+    keep = ~rt.near_tie
+    assert np.array_equal(idx[keep], rt.idx[keep])
+    dout64 = C.np64(dout)
+    for p in (0, cfg.n_priv - 1):
+        e = cfg.n_pub + p
+        hit = rt.idx == e
+        rows = np.nonzero(hit.any(axis=1))[0]
+        slot = np.argmax(hit[rows], axis=1)
+        gate = rt.gate[rows, slot].astype(np.float64)
+        _, dW13, dW2 = O.swiglu_backward(oi.x[rows], oi.w13_priv[p], oi.w2_priv[p],
+                                         gate[:, None] * dout64[rows])
+        e13 = C.rel_l2(g.dw13_priv[p].cpu().numpy(), dW13)
+        e2 = C.rel_l2(g.dw2_priv[p].cpu().numpy(), dW2)
+        log(f"  private expert {p}: {len(rows)} rows, rel_l2 dw13 {e13:.2e} dw2 {e2:.2e}")
+        assert e13 <= RTOL and e2 <= RTOL
+
+
 def test_backward_deterministic_and_public_weights_untouched():
     cfg = W.scaled_config(W.get_config("qwen"), **SMALL[0])
     dout = W.make_dout(cfg)
