@@ -43,7 +43,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "cd034d5d698ab77b4c7d8e726c6d26db55e08810929df7df5a74c83d480792e6": 1_989_802_093,
+    "388292c16f265b3d581b2485720c942a0e778310ae4eaff3161650057b6aa66a": 1_992_933_577,
 }
 
 

@@ -130,7 +130,9 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
 // are fixed, B is the group's weight matrix. K-ROWS mode: the contraction runs over the
 // group's rows (K = count[g]; rows past it are read as zeros), M and N are fixed, and
 // C is the group's own [M, N] matrix.
-enum { EPI_F32 = 0, EPI_SWIGLU_BWD = 1 };
+// EPI_SWIGLU_BWD also writes h for the weight gradient; EPI_SWIGLU_BWD_NOH (frozen
+// shared experts, no weight gradient) does not.
+enum { EPI_F32 = 0, EPI_SWIGLU_BWD = 1, EPI_SWIGLU_BWD_NOH = 2 };
 
 struct GemmArgs {
   const uint16_t* A;
@@ -346,7 +348,7 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
           const float db = v * ga * s;
           p.dA13[r * 2 * p.I + n] = (uint16_t)f32_to_bf16_rne(da);
           p.dA13[r * 2 * p.I + p.I + n] = (uint16_t)f32_to_bf16_rne(db);
-          if (p.Hh) p.Hh[r * p.I + n] = (uint16_t)f32_to_bf16_rne(ga * s * ub);
+          if (EPI == EPI_SWIGLU_BWD) p.Hh[r * p.I + n] = (uint16_t)f32_to_bf16_rne(ga * s * ub);
         }
       }
     }
@@ -545,7 +547,7 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     sh.B = (const uint16_t*)a.w2_sh; sh.ldb = a.Is;
     sh.C = nullptr; sh.N = a.Is; sh.K = H;
     sh.AB = a.AB_sh; sh.dA13 = a.dA13_sh; sh.Hh = nullptr; sh.I = a.Is;
-    e = launch_gemm<false, true, false, EPI_SWIGLU_BWD>(sh, mt * (sh.N / TN), s);
+    e = launch_gemm<false, true, false, EPI_SWIGLU_BWD_NOH>(sh, mt * (sh.N / TN), s);
     if (e != hipSuccess) return e;
     sh.A = a.dA13_sh; sh.lda = 2 * a.Is;
     sh.B = (const uint16_t*)a.w13_sh; sh.ldb = H;
