@@ -404,6 +404,12 @@ pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_t
  *                                               recomputes the pool logits; a token's
  *                                               pool is the one its selection lies in)
  *   w13_sh, w2_sh                               shared experts (n_shared > 0)
+ *   w2t_pub [n_pub, I, H], w13t_pub [n_pub, H, 2I], w2t_priv, w13t_priv
+ *                                               transposed expert weights
+ *                                               (pmpe_transpose_experts), all or none
+ *                                               (the private ones only when n_priv > 0):
+ *                                               with them the products with W2 and W13
+ *                                               run on the forward's grouped GEMM
  *   ab [T*k, 2I] fp32 or NULL                   the gate and up projections saved by
  *                                               pmpe_expert_ffn_train; NULL recomputes
  *                                               them (one more grouped GEMM)
@@ -428,7 +434,8 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
                           const float* wr_pub, const float* wr_priv, const void* w13_pub,
                           const void* w2_pub, const void* w13_priv, const void* w2_priv,
                           const float* logit_bias, const void* w13_sh, const void* w2_sh,
-                          const float* ab, float* dx, float* dw13_priv,
+                          const void* w2t_pub, const void* w13t_pub, const void* w2t_priv,
+                          const void* w13t_priv, const float* ab, float* dx, float* dw13_priv,
                           float* dw2_priv, float* dwr_priv, uint32_t* grad_rows, void* ws,
                           size_t ws_bytes, pmpe_stream_t stream);
 
@@ -451,6 +458,15 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
 pmpe_status pmpe_adamw(void* param, int32_t param_dtype, float* master, const float* grad,
                        float* m, float* v, uint64_t n, int32_t step, float lr, float beta1,
                        float beta2, float eps, float weight_decay, pmpe_stream_t stream);
+
+/*
+ * pmpe_transpose_experts - dst[e] = src[e]^T for n bf16 matrices of [rows, cols] (rows and
+ * cols multiples of 64, fewer than 2^31 elements each, n <= 65535, src and dst distinct
+ * and 16-byte aligned). Makes the transposed expert weights pmpe_backward can use; frozen
+ * public weights need it once, trained private weights after every optimizer step.
+ */
+pmpe_status pmpe_transpose_experts(const void* src, void* dst, int32_t n, int32_t rows,
+                                   int32_t cols, pmpe_stream_t stream);
 
 /*
  * pmpe_fingerprint - SHA-256 tree digest of a device buffer, to show that the frozen

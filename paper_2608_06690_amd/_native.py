@@ -108,7 +108,9 @@ _lib.pmpe_audit.argtypes = [_DESC, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]
 _lib.pmpe_backward_workspace_bytes.restype = _SZ
 _lib.pmpe_backward_workspace_bytes.argtypes = [_DESC, _I32]
 _lib.pmpe_backward.restype = _I32
-_lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 24 + [_P, _SZ, _P]
+_lib.pmpe_backward.argtypes = [_DESC, _I32] + [_P] * 28 + [_P, _SZ, _P]
+_lib.pmpe_transpose_experts.restype = _I32
+_lib.pmpe_transpose_experts.argtypes = [_P, _P, _I32, _I32, _I32, _P]
 _lib.pmpe_expert_ffn_train.restype = _I32
 _lib.pmpe_expert_ffn_train.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn_lora_workspace_bytes.restype = _SZ
@@ -131,7 +133,8 @@ EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_
             "pmpe_route", "pmpe_dispatch", "pmpe_expert_ffn", "pmpe_combine", "pmpe_audit",
             "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint", "pmpe_backward_workspace_bytes",
             "pmpe_backward", "pmpe_expert_ffn_train", "pmpe_route_record", "pmpe_cache_tag_check",
-            "pmpe_expert_ffn_lora_workspace_bytes", "pmpe_expert_ffn_lora", "pmpe_adamw"]
+            "pmpe_expert_ffn_lora_workspace_bytes", "pmpe_expert_ffn_lora", "pmpe_adamw",
+            "pmpe_transpose_experts"]
 
 PMPE_FP_LEAF_BYTES = 1024
 PMPE_FP_FANOUT = 16
@@ -238,13 +241,15 @@ def pmpe_expert_ffn_train(desc, T, x_perm, x, expert_count, expert_offset, row_t
 
 def pmpe_backward(desc, T, x, dout, topk_idx, topk_gate, expert_count, expert_offset, row_token,
                   token_row, y_perm, wr_pub, wr_priv, w13_pub, w2_pub, w13_priv, w2_priv,
-                  logit_bias, w13_sh, w2_sh, ab, dx, dw13_priv, dw2_priv, dwr_priv,
+                  logit_bias, w13_sh, w2_sh, w2t_pub, w13t_pub, w2t_priv, w13t_priv, ab, dx,
+                  dw13_priv, dw2_priv, dwr_priv,
                   grad_rows, ws, stream=None) -> None:
     _check(_lib.pmpe_backward(
         ctypes.byref(desc), T, _ptr(x), _ptr(dout), _ptr(topk_idx), _ptr(topk_gate),
         _ptr(expert_count), _ptr(expert_offset), _ptr(row_token), _ptr(token_row), _ptr(y_perm),
         _ptr(wr_pub), _ptr(wr_priv), _ptr(w13_pub), _ptr(w2_pub), _ptr(w13_priv), _ptr(w2_priv),
-        _ptr(logit_bias), _ptr(w13_sh), _ptr(w2_sh), _ptr(ab), _ptr(dx), _ptr(dw13_priv), _ptr(dw2_priv), _ptr(dwr_priv), _ptr(grad_rows), _ptr(ws),
+        _ptr(logit_bias), _ptr(w13_sh), _ptr(w2_sh), _ptr(w2t_pub), _ptr(w13t_pub),
+        _ptr(w2t_priv), _ptr(w13t_priv), _ptr(ab), _ptr(dx), _ptr(dw13_priv), _ptr(dw2_priv), _ptr(dwr_priv), _ptr(grad_rows), _ptr(ws),
         0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)), "pmpe_backward")
 
 
@@ -319,3 +324,12 @@ def pmpe_adamw(param: torch.Tensor, master: Optional[torch.Tensor], grad: torch.
     _check(_lib.pmpe_adamw(_ptr(param), dt, _ptr(master), _ptr(grad), _ptr(m), _ptr(v),
                            param.numel(), step, lr, beta1, beta2, eps, weight_decay,
                            _stream(stream)), "pmpe_adamw")
+
+
+def pmpe_transpose_experts(src: torch.Tensor, dst: torch.Tensor, stream=None) -> None:
+    """dst[e] = src[e]^T for a bf16 stack src [n, rows, cols] into dst [n, cols, rows]."""
+    n, rows, cols = src.shape
+    if tuple(dst.shape) != (n, cols, rows):
+        raise ValueError("dst must be [n, cols, rows]")
+    _check(_lib.pmpe_transpose_experts(_ptr(src), _ptr(dst), n, rows, cols, _stream(stream)),
+           "pmpe_transpose_experts")

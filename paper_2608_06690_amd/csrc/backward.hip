@@ -357,6 +357,34 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
 // ---------------------------------------------------------------------------
 // Reductions
 // ---------------------------------------------------------------------------
+// SwiGLU backward on the rows of dh (NT path): da = dh b s (1 + a (1 - s)),
+// db = dh a s, h = a s b, with [a; b] the saved fp32 gate and up projections; four
+// columns per thread.
+__global__ __launch_bounds__(BT) void bwd_swiglu_kernel(BwdArgs a, const float* AB) {
+  const int r = blockIdx.x, I = a.I;
+  const uint16_t* dh = a.dH + (size_t)r * I;
+  const float* ab = AB + (size_t)r * 2 * I;
+  uint16_t* da = a.dA13 + (size_t)r * 2 * I;
+  uint16_t* hh = a.Hh + (size_t)r * I;
+  for (int i = threadIdx.x * 4; i < I; i += BT * 4) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 dv = *(const u32x2*)(dh + i);
+    const f32x4 g = *(const f32x4*)(ab + i), u = *(const f32x4*)(ab + I + i);
+    float dga[4], dub[4], h[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float d = bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu);
+      const float s = 1.0f / (1.0f + __expf(-g[j]));
+      dga[j] = d * u[j] * s * (1.0f + g[j] * (1.0f - s));
+      dub[j] = d * g[j] * s;
+      h[j] = g[j] * s * u[j];
+    }
+    *(u32x2*)(da + i) = u32x2{pack_bf16x2(dga[0], dga[1]), pack_bf16x2(dga[2], dga[3])};
+    *(u32x2*)(da + I + i) = u32x2{pack_bf16x2(dub[0], dub[1]), pack_bf16x2(dub[2], dub[3])};
+    *(u32x2*)(hh + i) = u32x2{pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3])};
+  }
+}
+
 // Softmax over the whole permitted pool (POOL_SOFTMAX), block t: the pool logits
 // z_e = x_t . W_r[e] (+ b_e) are recomputed in fp32 (one wave per logit, fixed-order
 // reduction), p = softmax(z), and dz_e = p_e ([e selected] dg_e - sum_sel p_i dg_i) for
@@ -433,7 +461,15 @@ __global__ __launch_bounds__(BT) void bwd_dx_kernel(BwdArgs a) {
   for (int h = tid * 4; h < H; h += BT * 4) {
     f32x4 s = {0, 0, 0, 0};
     for (int j = 0; j < k; ++j) {
-      const f32x4 d = *(const f32x4*)(a.dXr + (size_t)s_r[j] * H + h);
+      f32x4 d;
+      if (a.w2t_pub) {  // NT path: bf16 row input gradients
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        const u32x2 v = *(const u32x2*)((const uint16_t*)a.dXr + (size_t)s_r[j] * H + h);
+        d = f32x4{bf16_to_f32(v[0] & 0xFFFFu), bf16_to_f32(v[0] >> 16), bf16_to_f32(v[1] & 0xFFFFu),
+                  bf16_to_f32(v[1] >> 16)};
+      } else {
+        d = *(const f32x4*)(a.dXr + (size_t)s_r[j] * H + h);
+      }
       const f32x4 w = *(const f32x4*)(s_w[j] + h);
       s += d + s_dz[j] * w;
     }
@@ -576,6 +612,30 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     AB = a.AB;
   }
+  if (a.w2t_pub) {  // host validation: all transposed weights or none
+    // NT path: dh = dY (W2^T)^T and the row input gradients = [da; db] (W13^T)^T on the
+    // forward's grouped GEMM (bf16 out), the SwiGLU backward as its own pass
+    FfnArgs f{};
+    f.T = a.T; f.k = a.k; f.n_pub = a.n_pub; f.n_priv = a.n_priv; f.act_bf16 = 1; f.Is = 0;
+    f.count = a.count; f.offset = a.offset; f.row_token = a.row_token;
+    f.H = I; f.I = H;  // N = I, K = H
+    f.w13_pub = f.w2_pub = a.w2t_pub;
+    f.w13_priv = f.w2_priv = a.w2t_priv;
+    f.h = (void*)a.dY;
+    f.y_perm = a.dH;
+    e = launch_grouped_nt_gemm(f, s);
+    if (e != hipSuccess) return e;
+    bwd_swiglu_kernel<<<R, BT, 0, s>>>(a, AB);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    f.H = H; f.I = 2 * I;  // N = H, K = 2I
+    f.w13_pub = f.w2_pub = a.w13t_pub;
+    f.w13_priv = f.w2_priv = a.w13t_priv;
+    f.h = a.dA13;
+    f.y_perm = a.dXr;  // bf16 rows in the fp32 buffer
+    e = launch_grouped_nt_gemm(f, s);
+    if (e != hipSuccess) return e;
+  } else {
   // dh = dY W2 (W2 stored [H, I]: K rows of N columns), SwiGLU backward in the epilogue
   g.A = a.dY; g.lda = H;
   g.B = (const uint16_t*)a.w2_pub; g.B_priv = (const uint16_t*)a.w2_priv;
@@ -591,6 +651,7 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
   g.C = a.dXr; g.ldc = H; g.N = H; g.K = 2 * I;
   e = launch_gemm<false, true, false, EPI_F32>(g, mt_max * (g.N / TN), s);
   if (e != hipSuccess) return e;
+  }
   if (a.n_priv > 0) {
     // dW2[p] = dY^T Hh over private expert p's rows: M = H, N = I
     GemmArgs w{};

@@ -195,8 +195,10 @@ struct TileInfo {
 // LDS-DMA as well, one tile ahead of their use, so no register-destined global load
 // inside the stream forces the compiler to drain the ring.
 // SAVE (GEMM1 only): also store the fp32 gate and up projections [a; b] of every routed
-// row into ab_save [T*k, 2I], for a later backward pass.
-template <class C, bool GATED, bool SAVE = false>
+// row into ab_save [T*k, 2I], for a later backward pass. AUDIT (GEMM2 only): count the
+// executed private rows; off when the kernel serves as a plain grouped GEMM (the
+// backward's products with transposed weights).
+template <class C, bool GATED, bool SAVE = false, bool AUDIT = true>
 __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
   __shared__ __attribute__((aligned(16))) int s_rt[3][C::BM];
@@ -271,7 +273,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   // Does tile t read row_token? (gathered x rows in GEMM1; the audit in GEMM2)
   auto needs_rt = [&](const TileInfo& t) {
     if (t.g >= E) return false;
-    return GATED ? (a.x_perm == nullptr) : (t.g >= a.n_pub);
+    return GATED ? (a.x_perm == nullptr) : (AUDIT && t.g >= a.n_pub);
   };
   const uint32_t lds0 = lds_addr(smem);
   const uint32_t rt0 = lds_addr(&s_rt[0][0]);
@@ -544,7 +546,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
       }
     }
     // Execution audit: the first N tile of every executed private M tile counts its rows.
-    if (!GATED && c_priv && c_valid && ct.n0 == 0) {
+    if (!GATED && AUDIT && c_priv && c_valid && ct.n0 == 0) {
       for (int r = tid; r < ct.rows; r += C::THREADS) atomicAdd(&a.audit_rows[s_rt[ci % 3][r]], 1u);
       if (ct.m0 == 0 && tid == 0 && a.audit_calls) atomicAdd(&a.audit_calls[ct.g - a.n_pub], 1u);
     }
@@ -708,6 +710,30 @@ __global__ __launch_bounds__(THREADS) void gemm2_f32_kernel(FfnArgs a, int share
 }  // namespace
 
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) { return launch_expert_ffn_parts(a, s, 3); }
+
+// The GEMM2 kernel as a plain grouped product without the audit: y[r] = h[r] W_g^T for the
+// rows of every routed group g, W_g [H, I] (K = I contiguous), bf16 in and out.
+hipError_t launch_grouped_nt_gemm(const FfnArgs& a, hipStream_t s) {
+  const int E = a.n_pub + a.n_priv;
+  int dev = 0, ncu = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ncu = v;
+  }
+  const bool large = (int64_t)a.T * a.k >= (int64_t)128 * E;
+  auto run = [&](auto cfg) {
+    using C = decltype(cfg);
+    int64_t tiles = ((int64_t)a.T * a.k / C::BM + E) * ((a.H + C::BN - 1) / C::BN);
+    int64_t g = (int64_t)ncu * C::PER_CU;
+    if (tiles < g) g = (tiles + 7) / 8 * 8;
+    hipLaunchKernelGGL((gemm_bf16_kernel<C, false, false, false>), dim3((unsigned)g), dim3(C::THREADS), 0, s, a);
+  };
+  if (large)
+    run(CfgLarge{});
+  else
+    run(CfgSmall{});
+  return hipGetLastError();
+}
 
 // parts: bit 0 runs GEMM1 (x -> h), bit 1 runs GEMM2 (h -> y)
 hipError_t launch_expert_ffn_parts(const FfnArgs& a, hipStream_t s, int parts) {

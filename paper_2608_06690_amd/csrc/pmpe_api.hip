@@ -75,7 +75,7 @@ pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR
 
 // backward workspace: Xp, dY, [a; b], h, [da; db], row input gradients, row dz
 struct BwdLayout {
-  size_t xp, dy, ab, hh, da, dxr, dz, part, dzp, absh, dash, dxsh, total;
+  size_t xp, dy, ab, hh, da, dxr, dz, part, dzp, absh, dash, dxsh, dh, total;
 };
 int bwd_pool_stride(const pmpe_layer_desc* d) {
   if (d->route_mode == PMPE_ROUTE_SOFT) return d->n_pub + d->n_priv;
@@ -98,6 +98,7 @@ BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
   L.absh = o; o += round_up(Tt * 2 * Is * 4);
   L.dash = o; o += round_up(Tt * 2 * Is * 2);
   L.dxsh = o; o += Is > 0 ? round_up(Tt * H * 4) : 0;
+  L.dh = o; o += round_up(R * I * 2);
   L.total = o;
   return L;
 }
@@ -107,6 +108,8 @@ pmpe_status check_backward_desc(const pmpe_layer_desc* d, int32_t T) {
   if (st != PMPE_OK) return st;
   if (d->act_dtype != PMPE_BF16) return PMPE_ERR_DTYPE;
   if (d->inter % 128 != 0) return PMPE_ERR_SHAPE;
+  // the grouped GEMMs address [T*k, 2I] rows with 32-bit element offsets
+  if ((int64_t)T * d->top_k * 2 * d->inter >= ((int64_t)1 << 31)) return PMPE_ERR_SHAPE;
   if (d->n_shared > 0 && ((int64_t)d->n_shared * d->shared_inter) % 128 != 0) return PMPE_ERR_SHAPE;
   // the pool-softmax pass stages one x row in fp32 LDS
   if (d->gate_mode == PMPE_GATE_POOL_SOFTMAX && d->hidden > 8192) return PMPE_ERR_SHAPE;
@@ -375,7 +378,8 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
                           const float* wr_pub, const float* wr_priv, const void* w13_pub,
                           const void* w2_pub, const void* w13_priv, const void* w2_priv,
                           const float* logit_bias, const void* w13_sh, const void* w2_sh,
-                          const float* ab, float* dx, float* dw13_priv,
+                          const void* w2t_pub, const void* w13t_pub, const void* w2t_priv,
+                          const void* w13t_priv, const float* ab, float* dx, float* dw13_priv,
                           float* dw2_priv, float* dwr_priv, uint32_t* grad_rows, void* ws,
                           size_t ws_bytes, pmpe_stream_t stream) {
   pmpe_status st = check_backward_desc(d, T);
@@ -386,7 +390,12 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
   if (d->n_priv > 0 && (!wr_priv || !w13_priv || !w2_priv || !dw13_priv || !dw2_priv || !dwr_priv))
     return PMPE_ERR_NULL;
   if (d->n_shared > 0 && (!w13_sh || !w2_sh)) return PMPE_ERR_NULL;
-  const void* al[] = {x, dout, y_perm, w13_pub, w2_pub, w13_priv, w2_priv, ab, w13_sh, w2_sh};
+  // transposed weights: all of them (private ones when there is a private pool) or none
+  const bool any_t = w2t_pub || w13t_pub || w2t_priv || w13t_priv;
+  if (any_t && (!w2t_pub || !w13t_pub || (d->n_priv > 0 && (!w2t_priv || !w13t_priv))))
+    return PMPE_ERR_NULL;
+  const void* al[] = {x, dout, y_perm, w13_pub, w2_pub, w13_priv, w2_priv, ab, w13_sh, w2_sh,
+                      w2t_pub, w13t_pub, w2t_priv, w13t_priv};
   for (const void* p : al)
     if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
   if (T == 0) return PMPE_OK;
@@ -403,7 +412,8 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
             bwd_pool_stride(d), logit_bias, (float*)(w + L.dzp),
             d->n_shared > 0 ? d->n_shared * d->shared_inter : 0, w13_sh, w2_sh,
             (float*)(w + L.absh), (uint16_t*)(w + L.dash),
-            d->n_shared > 0 ? (float*)(w + L.dxsh) : nullptr};
+            d->n_shared > 0 ? (float*)(w + L.dxsh) : nullptr,
+            any_t ? w2t_pub : nullptr, w13t_pub, w2t_priv, w13t_priv, (uint16_t*)(w + L.dh)};
   return launched(launch_backward(a, (hipStream_t)stream));
 }
 
@@ -424,6 +434,18 @@ pmpe_status pmpe_adamw(void* param, int32_t param_dtype, float* master, const fl
   const float c2 = (float)(1.0 - std::pow((double)beta2, (double)step));
   AdamwArgs a{param, master, grad, m, v, n, lr, beta1, beta2, eps, 1.0f - lr * weight_decay, c1, c2};
   return launched(launch_adamw(a, (hipStream_t)stream));
+}
+
+pmpe_status pmpe_transpose_experts(const void* src, void* dst, int32_t n, int32_t rows,
+                                   int32_t cols, pmpe_stream_t stream) {
+  if (n < 0 || n > 65535 || rows < 0 || cols < 0 || rows % 64 != 0 || cols % 64 != 0)
+    return PMPE_ERR_SHAPE;
+  if ((int64_t)rows * cols >= ((int64_t)1 << 31)) return PMPE_ERR_SHAPE;
+  if (n == 0 || rows == 0 || cols == 0) return PMPE_OK;
+  if (!src || !dst) return PMPE_ERR_NULL;
+  if (!aligned16(src) || !aligned16(dst)) return PMPE_ERR_ALIGN;
+  if (src == dst) return PMPE_ERR_SHAPE;
+  return launched(launch_transpose(src, dst, n, rows, cols, (hipStream_t)stream));
 }
 
 size_t pmpe_fingerprint_workspace_bytes(uint64_t nbytes) {

@@ -132,6 +132,7 @@ struct FfnArgs {
 };
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn_parts(const FfnArgs& a, hipStream_t s, int parts);
+hipError_t launch_grouped_nt_gemm(const FfnArgs& a, hipStream_t s);
 
 struct LoraArgs {
   int T, H, I, k, n_pub, n_priv, rank, gate;
@@ -239,10 +240,18 @@ struct BwdArgs {
   float* AB_sh;           // [T, 2 Is]
   uint16_t* dA13_sh;      // [T, 2 Is]
   float* dXsh;            // [T, H] or NULL
+  // transposed expert weights (K contiguous): W2^T [n, I, H], W13^T [n, H, 2I]; when all
+  // are present the dh and row-input-gradient products run on the grouped NT GEMM
+  const void* w2t_pub;
+  const void* w13t_pub;
+  const void* w2t_priv;
+  const void* w13t_priv;
+  uint16_t* dH;           // [T*k, I] bf16 (NT path)
 };
 constexpr int BWD_DWR_SPLIT = 16;  // row chunks per private expert in the router-row gradient
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t s);
+hipError_t launch_transpose(const void* src, void* dst, int n, int rows, int cols, hipStream_t s);
 
 // Fingerprint tree: 1 KiB leaves, 16 digests per inner node.
 constexpr uint32_t kFpLeafBytes = 1024;

@@ -186,18 +186,43 @@ class PolicyMaskedMoE:
                            torch.empty(max(N.pmpe_backward_workspace_bytes(d, T), 256),
                                        dtype=torch.uint8, device=dev))
 
+    def transposed_weights(self, stream=None):
+        """Transposed expert weights for the backward: the frozen public ones are made once
+        and kept; the private ones are remade on every call (training changes them)."""
+        if getattr(self, "_wt_pub", None) is None:
+            w2t = torch.empty(self.w2_pub.shape[0], self.w2_pub.shape[2], self.w2_pub.shape[1],
+                              dtype=self.w2_pub.dtype, device=self.device)
+            w13t = torch.empty(self.w13_pub.shape[0], self.w13_pub.shape[2], self.w13_pub.shape[1],
+                               dtype=self.w13_pub.dtype, device=self.device)
+            N.pmpe_transpose_experts(self.w2_pub, w2t, stream)
+            N.pmpe_transpose_experts(self.w13_pub, w13t, stream)
+            self._wt_pub = (w2t, w13t)
+        if self.w13_priv is None or self.desc.n_priv == 0:
+            return self._wt_pub + (None, None)
+        if getattr(self, "_wt_priv", None) is None:
+            self._wt_priv = (
+                torch.empty(self.w2_priv.shape[0], self.w2_priv.shape[2], self.w2_priv.shape[1],
+                            dtype=self.w2_priv.dtype, device=self.device),
+                torch.empty(self.w13_priv.shape[0], self.w13_priv.shape[2], self.w13_priv.shape[1],
+                            dtype=self.w13_priv.dtype, device=self.device))
+        N.pmpe_transpose_experts(self.w2_priv, self._wt_priv[0], stream)
+        N.pmpe_transpose_experts(self.w13_priv, self._wt_priv[1], stream)
+        return self._wt_pub + self._wt_priv
+
     def backward(self, x, dout, b: LayerBuffers, g: Optional[GradBuffers] = None,
-                 stream=None, use_saved: bool = True) -> GradBuffers:
+                 stream=None, use_saved: bool = True, transposed: bool = True) -> GradBuffers:
         """Private-only backward of the forward that filled `b` (same x): input gradient
         and the gradients of the private experts and private router rows. The gate and
         up projections saved by a training forward are used when present (and
-        `use_saved`), else recomputed."""
+        `use_saved`), else recomputed; with `transposed` the products with W2 and W13 use
+        transposed weight copies on the forward's grouped GEMM."""
         T = x.shape[0]
         g = g or self.grad_buffers(T)
+        wt = self.transposed_weights(stream) if transposed else (None, None, None, None)
         N.pmpe_backward(self.desc, T, x, dout, b.topk_idx, b.topk_gate, b.expert_count,
                         b.expert_offset, b.row_token, b.token_row, b.y_perm, self.wr_pub,
                         self.wr_priv, self.w13_pub, self.w2_pub, self.w13_priv, self.w2_priv,
-                        self.bias, self.w13_sh, self.w2_sh,
+                        self.bias, self.w13_sh, self.w2_sh, *wt,
                         b.ab if use_saved else None, g.dx, g.dw13_priv, g.dw2_priv, g.dwr_priv, g.grad_rows, g.ws, stream)
         return g
 

@@ -24,9 +24,10 @@ def log(msg):
     sys.stdout.flush()
 
 
-def forward_backward(cfg, soft=False, dout=None, saved=True):
+def forward_backward(cfg, soft=False, dout=None, saved=True, transposed=True):
     """Training forward (keeps the gate and up projections) then the backward, which
-    uses them (saved=True) or recomputes them."""
+    uses them (saved=True) or recomputes them, with transposed weight copies on the
+    grouped NT GEMM (transposed=True) or the transposing GEMM."""
     layer, Lw = C.device_layer(cfg, soft=soft)
     req = W.make_requests(cfg)
     words = O.compile_words(req.metas, req.lengths)
@@ -34,7 +35,7 @@ def forward_backward(cfg, soft=False, dout=None, saved=True):
     offs = torch.tensor(req.offsets, device="cuda")
     audit = layer.audit_buffers(cfg.tokens, len(req.offsets) - 1)
     b = layer.forward(x, C.words_tensor(words), audit, offs, train=True)
-    g = layer.backward(x, dout.to("cuda"), b, use_saved=saved)
+    g = layer.backward(x, dout.to("cuda"), b, use_saved=saved, transposed=transposed)
     torch.cuda.synchronize()
     return layer, Lw, b, g, words, x
 
@@ -60,16 +61,17 @@ SMALL = [
 
 
 @pytest.mark.parametrize("shape", SMALL, ids=lambda s: f"T{s['tokens']}_H{s['hidden']}_I{s['inter']}_k{s['top_k']}")
-@pytest.mark.parametrize("soft,saved", [(False, True), (False, False), (True, True)],
-                         ids=["masked", "masked-recompute", "soft"])
-def test_backward_matches_oracle(shape, soft, saved):
+@pytest.mark.parametrize("soft,saved,transposed", [(False, True, True), (False, False, True),
+                                                   (False, True, False), (True, True, True)],
+                         ids=["masked", "masked-recompute", "masked-transposing", "soft"])
+def test_backward_matches_oracle(shape, soft, saved, transposed):
     cfg = W.scaled_config(W.get_config("qwen"), **shape)
-    log(f"backward {shape} soft={soft} saved={saved}")
+    log(f"backward {shape} soft={soft} saved={saved} transposed={transposed}")
     oi = C.oracle_inputs(cfg)
     req = W.make_requests(cfg)
     words = O.compile_words(req.metas, req.lengths)
     rt, dout = oracle_route_and_dout(cfg, oi, words, soft)
-    layer, Lw, b, g, _, _ = forward_backward(cfg, soft, dout, saved)
+    layer, Lw, b, g, _, _ = forward_backward(cfg, soft, dout, saved, transposed)
     idx = b.topk_idx.view(cfg.tokens, cfg.top_k).cpu().numpy()
     keep = ~rt.near_tie
     assert np.array_equal(idx[keep], rt.idx[keep])
@@ -255,3 +257,13 @@ def test_backward_qwen_full_size_sampled_experts():
     if np.array_equal(idx, rt.idx):
         ref_rows = np.array([(rt.idx == cfg.n_pub + p).any(axis=1).sum() for p in range(cfg.n_priv)])
         assert np.array_equal(g.grad_rows.cpu().numpy(), ref_rows)
+
+
+@pytest.mark.parametrize("n,rows,cols", [(1, 64, 64), (3, 128, 192), (5, 2048, 768)])
+def test_transpose_experts(n, rows, cols):
+    g = torch.Generator(device="cuda").manual_seed(rows + cols)
+    src = torch.randn(n, rows, cols, device="cuda", generator=g).to(torch.bfloat16)
+    dst = torch.empty(n, cols, rows, device="cuda", dtype=torch.bfloat16)
+    P.pmpe_transpose_experts(src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(dst.cpu(), src.cpu().transpose(1, 2))
