@@ -267,3 +267,53 @@ def test_transpose_experts(n, rows, cols):
     P.pmpe_transpose_experts(src, dst)
     torch.cuda.synchronize()
     assert torch.equal(dst.cpu(), src.cpu().transpose(1, 2))
+
+
+@pytest.mark.parametrize("transposed", [True, False], ids=["nt", "transposing"])
+def test_backward_152_row_expert_and_empty_experts(transposed):
+    """The two cases the paper's FP8 preflight failed on: a reduction over an expert with
+    exactly 152 rows (not a multiple of the 64-row K step) and experts with no rows (their
+    gradients must be exactly zero). Planted route; private weight gradients against the
+    oracle's SwiGLU backward on each expert's rows."""
+    cfg = W.scaled_config(W.get_config("qwen"), tokens=400, requests=1, hidden=256, inter=128,
+                          n_pub=16, n_priv=8, top_k=2)
+    T, k = cfg.tokens, cfg.top_k
+    rng = np.random.default_rng(7)
+    idx = np.zeros((T, k), np.int64)
+    for t in range(T):
+        if t < 152:
+            idx[t] = [3, 20]                       # private expert 4 (id 20): exactly 152 rows
+        else:
+            idx[t] = np.sort(rng.choice([0, 1, 2, 5, 6, 17, 18], 2, replace=False))
+    gates = rng.random((T, k)).astype(np.float32)
+    layer, Lw = C.device_layer(cfg)
+    x = W.make_x(cfg, "cuda")
+    b = layer.buffers(T)
+    b.topk_idx.copy_(torch.from_numpy(idx.astype(np.int32).ravel()))
+    b.topk_gate.copy_(torch.from_numpy(gates.ravel()))
+    audit = layer.audit_buffers(T, 1)
+    layer.dispatch(x, b)
+    layer.expert_ffn(x, b, audit, train=True)
+    dout = W.make_dout(cfg)
+    g = layer.backward(x, dout.cuda(), b, transposed=transposed)
+    torch.cuda.synchronize()
+    count = b.expert_count.cpu().numpy()
+    assert count[20] == 152
+    oi = C.oracle_inputs(cfg)
+    d64 = C.np64(dout)
+    dw13 = g.dw13_priv.cpu().numpy()
+    dw2 = g.dw2_priv.cpu().numpy()
+    for p in range(cfg.n_priv):
+        e = cfg.n_pub + p
+        hit = idx == e
+        rows = np.nonzero(hit.any(axis=1))[0]
+        if len(rows) == 0:
+            assert not dw13[p].any() and not dw2[p].any()
+            assert not g.dwr_priv[p].any()
+            continue
+        slot = np.argmax(hit[rows], axis=1)
+        gt = gates[rows, slot].astype(np.float64)
+        _, r13, r2 = O.swiglu_backward(oi.x[rows], oi.w13_priv[p], oi.w2_priv[p], gt[:, None] * d64[rows])
+        assert C.rel_l2(dw13[p], r13) <= RTOL and C.rel_l2(dw2[p], r2) <= RTOL, p
+    assert np.isfinite(g.dx.cpu().numpy()).all()
+    assert np.array_equal(g.grad_rows.cpu().numpy().astype(np.int64), count[cfg.n_pub:])
