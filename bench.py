@@ -63,6 +63,8 @@ def parse():
     p.add_argument("--no-decode", action="store_true")
     p.add_argument("--no-fingerprint", action="store_true")
     p.add_argument("--no-backward", action="store_true")
+    p.add_argument("--no-fp8", action="store_true")
+    p.add_argument("--fp8-only", action="store_true", help="only time the fp8-weight variant")
     p.add_argument("--backward-only", action="store_true",
                    help="only time the private-only backward of the Qwen-shaped layer")
     p.add_argument("--vendor-gemm", action="store_true",
@@ -336,6 +338,58 @@ def backward_bench(args, dev):
     return res
 
 
+def fp8_bench(args, dev):
+    """Precision variant, not the bf16 metric: the expert FFN with fp8 (e4m3) weights and
+    power-of-two row scales, on the Qwen-shaped prefill layer and the decode batch (L2/MALL
+    flushed before each decode call)."""
+    import torch
+    import workloads as W
+    import paper_2608_06690_amd as P
+    res = {}
+    for wl in ("qwen", "decode"):
+        cfg, layer, x, words, req_off, audit, bufs, req = setup(wl, dev)
+        parts = [W.quantize_fp8_rows(t)[:2] for t in (layer.w13_pub, layer.w2_pub, layer.w13_priv, layer.w2_priv)]
+        fp8 = tuple(p[0] for p in parts) + tuple(p[1] for p in parts)
+        d8 = P.make_desc(cfg.hidden, cfg.inter, cfg.n_pub, cfg.n_priv, cfg.top_k)
+        d8.w_dtype = P.PMPE_FP8_E4M3
+        layer.route(x, words, bufs)
+        layer.dispatch(x, bufs)
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if wl == "decode" else None
+
+        def call():
+            P.pmpe_expert_ffn_fp8(d8, cfg.tokens, bufs.x_perm, x, bufs.expert_count,
+                                  bufs.expert_offset, bufs.row_token, *fp8, bufs.y_perm,
+                                  audit.token_rows, audit.priv_calls, bufs.dev_status, bufs.ws)
+
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(max(10, args.steps // 2)):
+            if flush is not None:
+                flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            call()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e3)
+        us = sum(times) / len(times)
+        counts = bufs.expert_count.cpu()
+        touched = int((counts > 0).sum())
+        wbytes = touched * 3 * cfg.hidden * cfg.inter  # one byte per weight
+        flop = cfg.tokens * cfg.top_k * 6 * cfg.hidden * cfg.inter
+        res[wl] = {"ffn_us_mean": us, "weight_bytes_fp8": wbytes,
+                   "weight_gbs": wbytes / (us * 1e-6) / 1e9,
+                   "weight_hbm_frac": wbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                   "tflops": flop / (us * 1e-6) / 1e12,
+                   "flushed": flush is not None}
+        del layer, x, bufs, fp8, parts, flush
+        torch.cuda.empty_cache()
+    return {"kind": "fp8 e4m3 expert weights with power-of-two row scales (precision "
+                    "variant; the metric line is bf16)", **res}
+
+
 def vendor_gemm_bench(dev, reps=20):
     """Context only: hipBLASLt (torch.bmm) on the Qwen layer's per-expert GEMM shapes with
     uniform rows (128 per public expert, 512 per private expert), without the SwiGLU, the
@@ -405,6 +459,9 @@ def main():
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
         return
+    if args.fp8_only:
+        print(json.dumps(fp8_bench(args, dev)), flush=True)
+        return
     if args.backward_only:
         print(json.dumps(backward_bench(args, dev)), flush=True)
         return
@@ -466,6 +523,8 @@ def main():
         out["backward"] = backward_bench(args, dev)
     if not args.no_fingerprint:
         out["fingerprint"] = fingerprint_bench(args, dev)
+    if not args.no_fp8:
+        out["fp8_weights"] = fp8_bench(args, dev)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, req, args.cpu_sample, args.cpu_reps)

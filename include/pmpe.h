@@ -61,7 +61,7 @@ typedef enum {
   PMPE_ERR_TAG_MISMATCH = -8     /* a cache tag does not match the request (reuse refused) */
 } pmpe_status;
 
-typedef enum { PMPE_F32 = 0, PMPE_BF16 = 1 } pmpe_dtype;
+typedef enum { PMPE_F32 = 0, PMPE_BF16 = 1, PMPE_FP8_E4M3 = 2 } pmpe_dtype;
 
 /* Gate normalisation (the paper does not fix it):
  * RENORM        softmax over the k selected logits (= pool softmax renormalised over
@@ -273,6 +273,30 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
                        const uint8_t* allow, const int32_t* req_offset, int32_t R,
                        uint64_t* req_private_rows, uint64_t* total_private_rows,
                        uint32_t* deny_violations, pmpe_stream_t stream);
+
+/*
+ * pmpe_expert_ffn_fp8 - pmpe_expert_ffn with expert weights stored as fp8 (OCP e4m3) and
+ * one fp32 scale per weight row that is a power of two: the weight is q * scale. A
+ * precision variant (the paper's models ran in bf16); activations, accumulation and
+ * outputs stay as in the bf16 path. Because the scales are powers of two and every e4m3
+ * value is exactly a bf16 value, the products equal those of the bf16 kernel on the
+ * dequantised weights; the weight bytes read from HBM halve.
+ *
+ *   d->act_dtype PMPE_BF16, d->w_dtype PMPE_FP8_E4M3, d->n_shared == 0
+ *   w13_* [n, 2I, H] and w2_* [n, H, I] fp8 bytes; w13s_* [n, 2I] and w2s_* [n, H] fp32
+ *   scales (NULL exactly when the matching private weights are NULL)
+ * Other arguments, the audit and the errors as pmpe_expert_ffn; PMPE_ERR_DTYPE for other
+ * dtypes, PMPE_ERR_SHAPE with shared experts. The scales are not checked on the device.
+ */
+pmpe_status pmpe_expert_ffn_fp8(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                                const void* x, const int32_t* expert_count,
+                                const int32_t* expert_offset, const int32_t* row_token,
+                                const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                                const void* w2_priv, const float* w13s_pub, const float* w2s_pub,
+                                const float* w13s_priv, const float* w2s_priv, void* y_perm,
+                                uint32_t* audit_token_rows, uint32_t* audit_priv_calls,
+                                uint32_t* dev_status, void* ws, size_t ws_bytes,
+                                pmpe_stream_t stream);
 
 /*
  * pmpe_expert_ffn_lora - the request-gated LoRA control arm (Sec. 4.2 matched expert-LoRA

@@ -12,7 +12,7 @@ from ._native import (PMPE_BF16, PMPE_F32, PMPE_GATE_POOL_SOFTMAX, PMPE_GATE_REN
                       make_cache_tag, pmpe_cache_tag_check, pmpe_route_record,
                       PMPE_LORA_GATE_POSTHOC, PMPE_LORA_GATE_ROW, PMPE_LORA_GATE_TILE,
                       PMPE_LORA_TILE_ROWS, pmpe_expert_ffn_lora, pmpe_expert_ffn_lora_workspace_bytes,
-                      pmpe_adamw, pmpe_transpose_experts,
+                      pmpe_adamw, pmpe_transpose_experts, PMPE_FP8_E4M3, pmpe_expert_ffn_fp8,
                       pmpe_audit, pmpe_check_desc, pmpe_combine, pmpe_dispatch, pmpe_expert_ffn,
                       pmpe_route, pmpe_version, pmpe_workspace_bytes)
 from .layer import (AuditBuffers, GradBuffers, LayerBuffers, PolicyMaskedMoE,  # noqa: F401

@@ -27,6 +27,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 PMPE_OK = 0
 PMPE_F32 = 0
 PMPE_BF16 = 1
+PMPE_FP8_E4M3 = 2
 PMPE_GATE_RENORM_TOPK = 0
 PMPE_GATE_POOL_SOFTMAX = 1
 PMPE_ROUTE_MASKED = 0
@@ -113,6 +114,8 @@ _lib.pmpe_transpose_experts.restype = _I32
 _lib.pmpe_transpose_experts.argtypes = [_P, _P, _I32, _I32, _I32, _P]
 _lib.pmpe_expert_ffn_train.restype = _I32
 _lib.pmpe_expert_ffn_train.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
+_lib.pmpe_expert_ffn_fp8.restype = _I32
+_lib.pmpe_expert_ffn_fp8.argtypes = [_DESC, _I32] + [_P] * 17 + [_P, _SZ, _P]
 _lib.pmpe_expert_ffn_lora_workspace_bytes.restype = _SZ
 _lib.pmpe_expert_ffn_lora_workspace_bytes.argtypes = [_DESC, _I32]
 _lib.pmpe_expert_ffn_lora.restype = _I32
@@ -134,7 +137,7 @@ EXPORTED = ["pmpe_version", "pmpe_status_string", "pmpe_workspace_bytes", "pmpe_
             "pmpe_fingerprint_workspace_bytes", "pmpe_fingerprint", "pmpe_backward_workspace_bytes",
             "pmpe_backward", "pmpe_expert_ffn_train", "pmpe_route_record", "pmpe_cache_tag_check",
             "pmpe_expert_ffn_lora_workspace_bytes", "pmpe_expert_ffn_lora", "pmpe_adamw",
-            "pmpe_transpose_experts"]
+            "pmpe_transpose_experts", "pmpe_expert_ffn_fp8"]
 
 PMPE_FP_LEAF_BYTES = 1024
 PMPE_FP_FANOUT = 16
@@ -333,3 +336,15 @@ def pmpe_transpose_experts(src: torch.Tensor, dst: torch.Tensor, stream=None) ->
         raise ValueError("dst must be [n, cols, rows]")
     _check(_lib.pmpe_transpose_experts(_ptr(src), _ptr(dst), n, rows, cols, _stream(stream)),
            "pmpe_transpose_experts")
+
+
+def pmpe_expert_ffn_fp8(desc, T, x_perm, x, expert_count, expert_offset, row_token, w13_pub,
+                        w2_pub, w13_priv, w2_priv, w13s_pub, w2s_pub, w13s_priv, w2s_priv, y_perm,
+                        audit_token_rows, audit_priv_calls, dev_status, ws, stream=None) -> None:
+    """Expert FFN with fp8 (e4m3, uint8 storage) weights and fp32 power-of-two row scales."""
+    _check(_lib.pmpe_expert_ffn_fp8(
+        ctypes.byref(desc), T, _ptr(x_perm), _ptr(x), _ptr(expert_count), _ptr(expert_offset),
+        _ptr(row_token), _ptr(w13_pub), _ptr(w2_pub), _ptr(w13_priv), _ptr(w2_priv),
+        _ptr(w13s_pub), _ptr(w2s_pub), _ptr(w13s_priv), _ptr(w2s_priv), _ptr(y_perm),
+        _ptr(audit_token_rows), _ptr(audit_priv_calls), _ptr(dev_status), _ptr(ws),
+        0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)), "pmpe_expert_ffn_fp8")

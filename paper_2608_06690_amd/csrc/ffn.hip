@@ -123,7 +123,7 @@ __device__ __forceinline__ int swz(int r, int c) {
 }
 
 template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_, int FRAG_BUFS_ = 1, bool HALF_ = true,
-          bool NT_B_ = false>
+          bool NT_B_ = false, bool W8_ = false>
 struct Cfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, BK = BK_;
   static constexpr int FRAG_BUFS = FRAG_BUFS_;  // 2: read the next K step's fragments early
@@ -134,17 +134,23 @@ struct Cfg {
   // (few rows per expert) this keeps the streamed weights from evicting the reused
   // activation rows (decode-shaped batch: 245 -> 185 us on MI355X).
   static constexpr bool NT_B = NT_B_;
+  // W8: expert weights are fp8 (e4m3) with a power-of-two scale per weight row; their
+  // LDS rows hold BK bytes and are widened to bf16 when the MFMA fragments are read.
+  static constexpr bool W8 = W8_;
   static constexpr int RB = 2 * BK, CH = BK / 8, RPD = 1024 / RB;  // rows per DMA instruction
+  static constexpr int RB_B = W8 ? BK : RB, CH_B = RB_B / 16, RPD_B = 1024 / RB_B;
   static constexpr int WAVES = WM * WN, THREADS = 64 * WAVES;
-  static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB, STAGE = A_BYTES + B_BYTES;
-  static constexpr int A_DMA = BM / RPD / WAVES, B_DMA = BN / RPD / WAVES;  // per wave per stage
+  static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB_B, STAGE = A_BYTES + B_BYTES;
+  static constexpr int A_DMA = BM / RPD / WAVES, B_DMA = BN / RPD_B / WAVES;  // per wave per stage
   // A wave owns MB 16-row blocks of the tile, interleaved with the other WM-1 row
   // waves (block j*WM + wm), so a partly filled tile loads every SIMD evenly.
   static constexpr int WROWS = BM / WM, MB = WROWS / 16;
   static constexpr int LDS = STAGES * STAGE;
-  static constexpr int PER_CU = (160 * 1024 - 8 * 1024) / LDS;  // resident blocks per CU
+  // resident blocks per CU: the ring plus up to 8 KiB of static tables per block
+  static constexpr int PER_CU = (160 * 1024) / (LDS + 8 * 1024);
   static_assert(BK == 32 || BK == 64, "BK");
-  static_assert(A_DMA * RPD * WAVES == BM && B_DMA * RPD * WAVES == BN, "DMA split");
+  static_assert(A_DMA * RPD * WAVES == BM && B_DMA * RPD_B * WAVES == BN, "DMA split");
+  static_assert(!W8 || BK == 64, "fp8 weight rows are 64 bytes");
 };
 #ifndef PMPE_CFG_LARGE
 #define PMPE_CFG_LARGE 256, 256, 4, 2, 2, 64
@@ -154,6 +160,16 @@ struct Cfg {
 #endif
 using CfgLarge = Cfg<PMPE_CFG_LARGE>;  // prefill: 8 waves of 64 x 128, 2 x 64 KiB stages
 using CfgSmall = Cfg<PMPE_CFG_SMALL>;  // decode-shaped: 4 waves, 3 x 24 KiB stages, streamed weights
+// fp8 weights: the smaller weight tiles leave room for a third stage (3 x 48 KiB) in the
+// prefill configuration and for three resident blocks per CU in the decode one
+#ifndef PMPE_CFG_LARGE8
+#define PMPE_CFG_LARGE8 256, 256, 4, 2, 3, 64, 1, true, false, true
+#endif
+#ifndef PMPE_CFG_SMALL8
+#define PMPE_CFG_SMALL8 64, 128, 1, 4, 3, 64, 2, true, true, true
+#endif
+using CfgLarge8 = Cfg<PMPE_CFG_LARGE8>;
+using CfgSmall8 = Cfg<PMPE_CFG_SMALL8>;
 
 constexpr int MAXG = 2 * PMPE_MAX_POOL + 1;  // routed experts + the shared group
 
@@ -292,28 +308,35 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   constexpr int CHK = C::CH;
   const int lrow = lane / CHK, lphys = lane % CHK;
   auto logical = [&](int r) { return (BK == 64) ? (lphys ^ (r & 7)) : (lphys ^ ((r >> 1) & 3)); };
+  // weight rows of RB_B bytes (fp8: 64-byte rows, the 64-byte-row swizzle)
+  const int lrow_b = lane / C::CH_B, lphys_b = lane % C::CH_B;
+  auto logical_b = [&](int r) {
+    if constexpr (C::W8) return lphys_b ^ ((r >> 1) & 3);
+    else return logical(r);
+  };
+  constexpr int ESZ = C::W8 ? 1 : 2;  // bytes per weight element
   // Copy sources as 32-bit element offsets from tile-uniform bases (the host checks
   // that every offset fits).
   uint32_t offA[C::A_DMA], offB[C::B_DMA];
   const uint16_t* baseA = nullptr;
-  const uint16_t* baseB = nullptr;
+  const unsigned char* baseB = nullptr;  // weight bytes
   bool p_valid = true;  // producer tile has weights (private tiles may not)
   auto setup_ctx = [&](const TileInfo& t, int slot) {
     const bool shared = t.g >= E;
     const bool priv = !shared && t.g >= a.n_pub;
     const int I = shared ? a.Is : a.I;
     const int K = GATED ? H : I;
-    const uint16_t* w;
+    const unsigned char* w;
     if (shared) {
-      w = (const uint16_t*)(GATED ? a.w13_sh : a.w2_sh);
+      w = (const unsigned char*)(GATED ? a.w13_sh : a.w2_sh);
     } else if (!priv) {
-      w = (const uint16_t*)(GATED ? a.w13_pub : a.w2_pub) + (size_t)t.g * (GATED ? 2 : 1) * I * H;
+      w = (const unsigned char*)(GATED ? a.w13_pub : a.w2_pub) + (size_t)t.g * (GATED ? 2 : 1) * I * H * ESZ;
     } else {
-      w = (const uint16_t*)(GATED ? a.w13_priv : a.w2_priv);
-      if (w) w += (size_t)(t.g - a.n_pub) * (GATED ? 2 : 1) * I * H;
+      w = (const unsigned char*)(GATED ? a.w13_priv : a.w2_priv);
+      if (w) w += (size_t)(t.g - a.n_pub) * (GATED ? 2 : 1) * I * H * ESZ;
     }
     p_valid = (w != nullptr) && !(priv && (a.w13_priv == nullptr || a.w2_priv == nullptr));
-    if (!p_valid) w = (const uint16_t*)(GATED ? a.w13_pub : a.w2_pub);  // read but never used
+    if (!p_valid) w = (const unsigned char*)(GATED ? a.w13_pub : a.w2_pub);  // read but never used
     if (GATED)
       baseA = (const uint16_t*)((!shared && a.x_perm) ? a.x_perm : a.x);
     else
@@ -336,7 +359,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < C::B_DMA; ++i) {
-      const int r = (uwave * C::B_DMA + i) * C::RPD + lrow;
+      const int r = (uwave * C::B_DMA + i) * C::RPD_B + lrow_b;
       int wrow;
       if (GATED) {
         const int half = C::BN / 2;
@@ -346,7 +369,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
       } else {
         wrow = min(t.n0 + r, H - 1);
       }
-      offB[i] = ((uint32_t)wrow * (uint32_t)K + logical(r) * 8) * 2;  // bytes
+      offB[i] = ((uint32_t)wrow * (uint32_t)K + logical_b(r) * (16 / ESZ)) * ESZ;  // bytes
     }
     return K / BK;
   };
@@ -355,7 +378,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     const uint32_t sa = __builtin_amdgcn_readfirstlane(lds0 + slot * C::STAGE);
     const uint32_t sb = sa + C::A_BYTES;
     const uint16_t* ba = baseA + k0;  // scalar bases advance by the K step
-    const uint16_t* bb = baseB + k0;
+    const unsigned char* bb = baseB + k0 * ESZ;
     const uint32_t wa = sa + uwave * C::A_DMA * 1024, wb = sb + uwave * C::B_DMA * 1024;
     Unroll<0, C::A_DMA>::run([&](auto i) { dma16s<i.value * 1024, false>(offA[i.value], ba, wa); });
     Unroll<0, C::B_DMA>::run([&](auto i) { dma16s<i.value * 1024, C::NT_B>(offB[i.value], bb, wb); });
@@ -401,17 +424,37 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   // Every operand block starts at a multiple of 16 rows, so the swizzled position of a
   // lane's chunk depends on the lane alone: one per-lane offset per K sub-step, plus a
   // wave-uniform part, plus a compile-time part that fits the ds_read offset field.
-  uint32_t lane_off[SUB];
+  uint32_t lane_off[SUB], lane_off_b[SUB];
 #pragma unroll
-  for (int sub = 0; sub < SUB; ++sub) lane_off[sub] = (uint32_t)swz<BK>(lane & 15, sub * 4 + (lane >> 4));
+  for (int sub = 0; sub < SUB; ++sub) {
+    lane_off[sub] = (uint32_t)swz<BK>(lane & 15, sub * 4 + (lane >> 4));
+    // fp8 weights: 8 bytes (8 K values) per lane, half a 16-byte chunk of a 64-byte row
+    lane_off_b[sub] = C::W8 ? (uint32_t)(swz<32>(lane & 15, sub * 2 + (lane >> 5)) + 8 * ((lane >> 4) & 1))
+                            : lane_off[sub];
+  }
   // Fragments of K sub-step `sub`: all NB operand blocks of B, and the first MBL
   // 16-row blocks of A (the blocks past MBL hold no valid row of the tile).
   auto read_frags = [&](auto mbl, int slot, int sub, int buf) {
     constexpr int MBL = decltype(mbl)::value;
     const uint32_t pa = lane_off[sub] + slot * C::STAGE + arow(0) * C::RB;
-    const uint32_t pb = lane_off[sub] + slot * C::STAGE + C::A_BYTES + wn * WCOLS * C::RB;
+    const uint32_t pb = lane_off_b[sub] + slot * C::STAGE + C::A_BYTES + wn * WCOLS * C::RB_B;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) fb[buf][nb] = as_bf16x8(*(const u32x4*)(smem + pb + bconst(nb) * C::RB));
+    for (int nb = 0; nb < NB; ++nb) {
+      if constexpr (C::W8) {
+        // 8 fp8 values widened exactly to bf16 (scale 1; the row scale is applied to the
+        // fp32 accumulators in the epilogue)
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        typedef __bf16 b16x2 __attribute__((ext_vector_type(2)));
+        const u32x2 q = *(const u32x2*)(smem + pb + bconst(nb) * C::RB_B);
+        const b16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q.x, 1.0f, false);
+        const b16x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q.x, 1.0f, true);
+        const b16x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q.y, 1.0f, false);
+        const b16x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(q.y, 1.0f, true);
+        fb[buf][nb] = bf16x8{p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
+      } else {
+        fb[buf][nb] = as_bf16x8(*(const u32x4*)(smem + pb + bconst(nb) * C::RB));
+      }
+    }
 #pragma unroll
     for (int mb = 0; mb < MBL; ++mb)
       fa[buf][mb] = as_bf16x8(*(const u32x4*)(smem + pa + mb * C::WM * 16 * C::RB));
@@ -471,6 +514,14 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     // Epilogue through the ring slot just consumed (younger slots hold the next
     // tile's operands in flight).
     uint16_t* so = (uint16_t*)(smem + ((gs - 1) % S) * C::STAGE);
+    // fp8 weights: the per-row scales of this tile's expert (powers of two, so scaling
+    // the fp32 accumulators equals multiplying by the dequantised weights)
+    const float* sc = nullptr;
+    if constexpr (C::W8) {
+      const int rows_w = GATED ? 2 * width : width;
+      sc = (ct.g < a.n_pub) ? (GATED ? a.w13_scale_pub : a.w2_scale_pub) + (size_t)ct.g * rows_w
+                            : (GATED ? a.w13_scale_priv : a.w2_scale_priv) + (size_t)(ct.g - a.n_pub) * rows_w;
+    }
     for (int pass = 0; pass < C::BM / ER; ++pass) {
       barrier_raw();  // the slot's previous contents are no longer read
 #pragma unroll
@@ -478,12 +529,19 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
         const int r0 = arow(mb);
         if (r0 / ER == pass && mb < mb_live) {
 #pragma unroll
-          for (int nb = 0; nb < NBO; ++nb)
+          for (int nb = 0; nb < NBO; ++nb) {
+            float sg = 1.0f, su = 1.0f;
+            if constexpr (C::W8) {
+              const int col = min(ct.n0 + wn * WCOLS + nb * 16 + (lane & 15), width - 1);
+              sg = sc[col];
+              if (GATED) su = sc[width + col];
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int r = r0 - pass * ER + (lane >> 4) * 4 + i;
               const int c = wn * WCOLS + nb * 16 + (lane & 15);
-              const float v = GATED ? silu(acc[mb][nb][i]) * acc[mb][nb + NBO][i] : acc[mb][nb][i];
+              const float v = GATED ? silu(acc[mb][nb][i] * sg) * (acc[mb][nb + NBO][i] * su)
+                                    : acc[mb][nb][i] * sg;
               so[r * NCOLS + c] = (uint16_t)f32_to_bf16_rne(v);
               if constexpr (GATED && SAVE) {
                 const int rt = r0 + (lane >> 4) * 4 + i;  // row within the tile
@@ -495,6 +553,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
                 }
               }
             }
+          }
         }
       }
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes landed
@@ -710,6 +769,34 @@ __global__ __launch_bounds__(THREADS) void gemm2_f32_kernel(FfnArgs a, int share
 }  // namespace
 
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) { return launch_expert_ffn_parts(a, s, 3); }
+
+// fp8 expert weights (routed experts only, no shared group): the same two GEMMs.
+hipError_t launch_expert_ffn_fp8(const FfnArgs& a, hipStream_t s) {
+  const int E = a.n_pub + a.n_priv;
+  int dev = 0, ncu = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ncu = v;
+  }
+  const bool large = (int64_t)a.T * a.k >= (int64_t)128 * E;
+  auto run = [&](auto cfg) {
+    using C = decltype(cfg);
+    auto grid = [&](int ncols, bool gemm1) {
+      const int64_t w = gemm1 ? a.I : a.H;
+      int64_t tiles = ((int64_t)a.T * a.k / C::BM + E) * ((w + ncols - 1) / ncols);
+      int64_t g = (int64_t)ncu * C::PER_CU;
+      if (tiles < g) g = (tiles + 7) / 8 * 8;
+      return dim3((unsigned)g);
+    };
+    hipLaunchKernelGGL((gemm_bf16_kernel<C, true>), grid(C::BN / 2, true), dim3(C::THREADS), 0, s, a);
+    hipLaunchKernelGGL((gemm_bf16_kernel<C, false>), grid(C::BN, false), dim3(C::THREADS), 0, s, a);
+  };
+  if (large)
+    run(CfgLarge8{});
+  else
+    run(CfgSmall8{});
+  return hipGetLastError();
+}
 
 // The GEMM2 kernel as a plain grouped product without the audit: y[r] = h[r] W_g^T for the
 // rows of every routed group g, W_g [H, I] (K = I contiguous), bf16 in and out.

@@ -287,6 +287,42 @@ pmpe_status pmpe_audit(const pmpe_layer_desc* d, int32_t T, const uint32_t* audi
   return launched(launch_audit(a, (hipStream_t)stream));
 }
 
+pmpe_status pmpe_expert_ffn_fp8(const pmpe_layer_desc* d, int32_t T, const void* x_perm,
+                                const void* x, const int32_t* expert_count,
+                                const int32_t* expert_offset, const int32_t* row_token,
+                                const void* w13_pub, const void* w2_pub, const void* w13_priv,
+                                const void* w2_priv, const float* w13s_pub, const float* w2s_pub,
+                                const float* w13s_priv, const float* w2s_priv, void* y_perm,
+                                uint32_t* audit_token_rows, uint32_t* audit_priv_calls,
+                                uint32_t* dev_status, void* ws, size_t ws_bytes,
+                                pmpe_stream_t stream) {
+  if (!d) return PMPE_ERR_NULL;
+  if (d->act_dtype != PMPE_BF16 || d->w_dtype != PMPE_FP8_E4M3) return PMPE_ERR_DTYPE;
+  // the descriptor checks of the bf16 path, with the weight dtype read as bf16
+  pmpe_layer_desc db = *d;
+  db.w_dtype = PMPE_BF16;
+  pmpe_status st = check_desc(&db, T);
+  if (st != PMPE_OK) return st;
+  if (d->n_shared != 0) return PMPE_ERR_SHAPE;
+  if (!expert_count || !expert_offset || !row_token || !w13_pub || !w2_pub || !y_perm ||
+      !audit_token_rows || !w13s_pub || !w2s_pub)
+    return PMPE_ERR_NULL;
+  if (!x_perm && !x) return PMPE_ERR_NULL;
+  if ((w13_priv != nullptr) != (w13s_priv != nullptr) || (w2_priv != nullptr) != (w2s_priv != nullptr))
+    return PMPE_ERR_NULL;
+  const void* al[] = {x_perm, x, w13_pub, w2_pub, w13_priv, w2_priv, y_perm};
+  for (const void* p : al)
+    if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
+  if (T == 0) return PMPE_OK;
+  if (!ws || ws_bytes < ffn_ws(&db, T)) return PMPE_ERR_WORKSPACE;
+  if (!aligned16(ws)) return PMPE_ERR_ALIGN;
+  FfnArgs a{T, d->hidden, d->inter, d->n_pub, d->n_priv, d->top_k, 1, 0, x_perm, x, expert_count,
+            expert_offset, row_token, w13_pub, w2_pub, w13_priv, w2_priv, nullptr, nullptr, nullptr,
+            y_perm, audit_token_rows, audit_priv_calls, dev_status, ws, nullptr, nullptr,
+            w13s_pub, w2s_pub, w13s_priv, w2s_priv};
+  return launched(launch_expert_ffn_fp8(a, (hipStream_t)stream));
+}
+
 size_t pmpe_expert_ffn_lora_workspace_bytes(const pmpe_layer_desc* d, int32_t T) {
   if (check_desc(d, T) != PMPE_OK) return 0;
   return ffn_ws(d, T) + round_up((size_t)T * d->top_k * 2 * d->inter * 4);

@@ -129,10 +129,16 @@ struct FfnArgs {
   void* h;     // workspace [T*k, I]
   void* h_sh;  // workspace [T, Is]
   float* ab_save = nullptr;  // optional [T*k, 2I]: fp32 gate and up projections (bf16 path)
+  // fp8 (e4m3) expert weights: fp32 power-of-two scale per weight row, [n, 2I] and [n, H]
+  const float* w13_scale_pub = nullptr;
+  const float* w2_scale_pub = nullptr;
+  const float* w13_scale_priv = nullptr;
+  const float* w2_scale_priv = nullptr;
 };
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn_parts(const FfnArgs& a, hipStream_t s, int parts);
 hipError_t launch_grouped_nt_gemm(const FfnArgs& a, hipStream_t s);
+hipError_t launch_expert_ffn_fp8(const FfnArgs& a, hipStream_t s);
 
 struct LoraArgs {
   int T, H, I, k, n_pub, n_priv, rank, gate;

@@ -162,6 +162,25 @@ class PolicyMaskedMoE:
             self.audit(T, b, audit, req_offset, stream)
         return b
 
+    def forward_fp8(self, x, words, fp8, audit: AuditBuffers, req_offset=None,
+                    stream=None) -> LayerBuffers:
+        """The layer with fp8 expert weights: fp8 = (w13_pub, w2_pub, w13_priv, w2_priv,
+        w13s_pub, w2s_pub, w13s_priv, w2s_priv) (uint8 weights, fp32 row scales); routing,
+        dispatch, combine and audit as in forward()."""
+        T = x.shape[0]
+        b = self.buffers(T)
+        self.route(x, words, b, stream)
+        self.dispatch(x, b, stream)
+        d8 = N.LayerDesc(*[getattr(self.desc, f) for f, _ in N.LayerDesc._fields_])
+        d8.w_dtype = N.PMPE_FP8_E4M3
+        N.pmpe_expert_ffn_fp8(d8, T, b.x_perm, x, b.expert_count, b.expert_offset, b.row_token,
+                              *fp8, b.y_perm, audit.token_rows, audit.priv_calls, b.dev_status,
+                              b.ws, stream)
+        self.combine(x, b, stream)
+        if req_offset is not None:
+            self.audit(T, b, audit, req_offset, stream)
+        return b
+
     def route_record(self, T: int, b: LayerBuffers, req_offset, layer: int = 0,
                      rec: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
         """Route records of the last forward of this T: [T, 4] int32 (pmpe_route_rec)."""

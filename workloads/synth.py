@@ -260,6 +260,20 @@ def make_lora(cfg: LayerConfig, rank: int, layer: int = 0, device="cpu", std: fl
             normal(k(T_LORA_B2), (n, H, rank), std, dt, device))
 
 
+def quantize_fp8_rows(w: torch.Tensor):
+    """Per-row power-of-two scaling of a weight stack [..., rows, cols] into OCP fp8 e4m3:
+    scale = 2^ceil(log2(max|row| / 448)) (1 for an all-zero row), q = round-to-nearest-even
+    of w / scale. Returns (q as uint8 bytes, fp32 scales [..., rows], the dequantised
+    weights q * scale as fp32); q * scale is exact, and so is its bf16 value."""
+    wf = w.float()
+    amax = wf.abs().amax(dim=-1)
+    e = torch.ceil(torch.log2(torch.clamp(amax, min=1e-30) / 448.0))
+    scale = torch.where(amax > 0, torch.exp2(e), torch.ones_like(amax))
+    q = (wf / scale.unsqueeze(-1)).to(torch.float8_e4m3fn)
+    deq = q.float() * scale.unsqueeze(-1)
+    return q.view(torch.uint8), scale.contiguous(), deq
+
+
 def make_router(cfg: LayerConfig, layer: int = 0, device="cpu"):
     s = cfg.seed
     wr_pub = normal(tensor_key(s, layer, T_WR_PUB, 0), (cfg.n_pub, cfg.hidden), cfg.wr_std,
