@@ -239,3 +239,25 @@ def test_adamw_validation():
     assert call(0x1004, 0, None, 16, 1) == -5
     assert call(None, 0, None, 0, 1) == 0              # nothing to do
     del a, ok
+
+
+def test_fp8_entry_validation():
+    lib = N.lib()
+    d = desc()
+    ptrs = [0x1000 * (i + 1) for i in range(17)]
+    # bf16 weights through the fp8 entry: dtype error
+    assert lib.pmpe_expert_ffn_fp8(ctypes.byref(d), 16, *ptrs, 0x20000, 1 << 20, None) == -4
+    d8 = desc()
+    d8.w_dtype = N.PMPE_FP8_E4M3
+    # the bf16 entry refuses fp8 weights
+    assert lib.pmpe_expert_ffn(ctypes.byref(d8), 16, *([0x1000] * 16), 0x20000, 1 << 20, None) == -4
+    # shared experts are not supported with fp8 weights
+    ds = desc(n_shared=2, shared_inter=256)
+    ds.w_dtype = N.PMPE_FP8_E4M3
+    assert lib.pmpe_expert_ffn_fp8(ctypes.byref(ds), 16, *ptrs, 0x20000, 1 << 20, None) == -2
+    # private weights without their scales
+    p2 = list(ptrs)
+    p2[11] = None  # w13s_priv
+    assert lib.pmpe_expert_ffn_fp8(ctypes.byref(d8), 16, *p2, 0x20000, 1 << 20, None) == -1
+    # workspace too small
+    assert lib.pmpe_expert_ffn_fp8(ctypes.byref(d8), 16, *ptrs, 0x20000, 16, None) == -6
