@@ -167,6 +167,32 @@ def time_layer(layer, x, words, req_off, audit, bufs, steps, warmup, flush=None)
     return wall / steps * 1e3, med, mean, p10, p90
 
 
+def call_bytes(cfg, counts, T, any_allow, any_deny):
+    """Algorithmic HBM bytes of each call of one layer pass (reads plus writes)."""
+    H, k, E = cfg.hidden, cfg.top_k, cfg.n_pub + cfg.n_priv
+    el = 2 if cfg.dtype == "bf16" else 4
+    pairs = T * k
+    touched = int((counts > 0).sum())
+    return {
+        # x, the permitted router rows, policy words; idx, gates, allow, kgap out
+        "route": T * H * el + (cfg.n_pub * H * 4 if any_deny else 0)
+                 + (cfg.n_priv * H * 4 if any_allow else 0) + T * 4 + pairs * 8 + T * 5,
+        # idx in; counts, offsets, row_token, token_row out
+        "dispatch": pairs * 4 + E * 8 + 4 + pairs * 8,
+        # touched experts' weights once, x rows in, y rows out
+        "expert_ffn": touched * 3 * H * cfg.inter * el + pairs * H * el * 2,
+        # y rows, token_row and gates in; out
+        "combine": pairs * H * el + pairs * 8 + T * H * el,
+        # per-token counts and decisions in; per-request sums out
+        "audit": T * 5 + (cfg.requests + 1) * 4 + cfg.requests * 8 + 12,
+    }
+
+
+def kernel_rates(nbytes, us):
+    return {c: {"bytes": nbytes[c], "us": us[c], "gbs": nbytes[c] / (us[c] * 1e-6) / 1e9,
+                "hbm_frac": nbytes[c] / (us[c] * 1e-6) / 1e9 / PEAK_HBM_GBS} for c in CALLS}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -238,6 +264,9 @@ def decode_bench(args, dev):
            "ffn_hbm_frac": gbs / PEAK_HBM_GBS, "calls_us_mean": meand,
            "calls_us_median": medd, "calls_us_p10": p10d, "calls_us_p90": p90d,
            "note": "L2/MALL flushed by a 512 MiB write before each event-timed step"}
+    al = bd.allow.cpu()
+    res["calls_hbm"] = kernel_rates(call_bytes(cfgd, counts, cfgd.tokens, bool(al.any()),
+                                               bool((al == 0).any())), meand)
     del layerd, xd, bd, flush
     torch.cuda.empty_cache()
     return res
@@ -514,6 +543,9 @@ def main():
                      "attainable_frac": achieved / attainable},
         "calls_us_mean": mean, "calls_us_median": med, "calls_us_p10": p10, "calls_us_p90": p90,
     }
+    allow = bufs.allow.cpu()
+    out["calls_hbm"] = kernel_rates(call_bytes(cfg, bufs.expert_count.cpu(), T, bool(allow.any()),
+                                               bool((allow == 0).any())), mean)
     del layer, x, bufs
     torch.cuda.empty_cache()
 

@@ -41,7 +41,8 @@ __global__ __launch_bounds__(64 * AU_WAVES) void audit_kernel(AuditArgs a) {
     const int hi = min(max(a.req_offset[r + 1], lo), a.T);
     unsigned long long sum = 0;
     unsigned int viol = 0;
-    for (int t = lo + lane; t < hi; t += 64) {
+#pragma unroll 8
+    for (int t = lo + lane; t < hi; t += 64) {  // unrolled: several loads in flight per lane
       const uint32_t v = a.rows[t];
       sum += v;
       viol += (a.allow[t] == 0 && v > 0) ? 1u : 0u;
