@@ -64,6 +64,10 @@ def parse():
     p.add_argument("--no-fingerprint", action="store_true")
     p.add_argument("--no-backward", action="store_true")
     p.add_argument("--no-fp8", action="store_true")
+    p.add_argument("--no-deepseek", action="store_true")
+    p.add_argument("--stack", action="store_true",
+                   help="also time the 48-layer stack (72.5 GB of weights, about a minute)")
+    p.add_argument("--stack-only", action="store_true", help="only time the 48-layer stack")
     p.add_argument("--fp8-only", action="store_true", help="only time the fp8-weight variant")
     p.add_argument("--backward-only", action="store_true",
                    help="only time the private-only backward of the Qwen-shaped layer")
@@ -268,6 +272,97 @@ def decode_bench(args, dev):
     res["calls_hbm"] = kernel_rates(call_bytes(cfgd, counts, cfgd.tokens, bool(al.any()),
                                                bool((al == 0).any())), meand)
     del layerd, xd, bd, flush
+    torch.cuda.empty_cache()
+    return res
+
+
+def deepseek_bench(args, dev):
+    """The DeepSeek-V2-Lite-shaped layer (8192 tokens, 2 shared + 64 public + 16 private
+    experts of intermediate 1408, top-6, pool softmax, N(0,1) logit bias): tokens/s and
+    the expert FFN's MFMA fraction (routed and shared experts)."""
+    import torch
+    cfg, layer, x, words, req_off, audit, bufs, req = setup("deepseek", dev)
+    ms, med, mean, p10, p90 = time_layer(layer, x, words, req_off, audit, bufs,
+                                         max(10, args.steps // 2), args.warmup)
+    pairs = cfg.tokens * cfg.top_k
+    flop = 6 * cfg.hidden * (pairs * cfg.inter + cfg.tokens * cfg.n_shared * cfg.shared_inter)
+    tf = flop / (mean["expert_ffn"] * 1e-6) / 1e12
+    al = bufs.allow.cpu()
+    counts = bufs.expert_count.cpu()
+    res = {"workload": "deepseek-v2-lite-shaped layer, 16 requests x 512 tokens, allow/deny at 0.5",
+           "tokens_per_s": cfg.tokens / (ms * 1e-3), "ms_per_step": ms,
+           "experts_empty": int((counts == 0).sum()), "ffn_flop": flop, "ffn_us_mean": mean["expert_ffn"],
+           "ffn_tflops": tf, "ffn_mfma_frac": tf / PEAK_BF16_TFLOPS, "calls_us_mean": mean,
+           "calls_us_p10": p10, "calls_us_p90": p90,
+           "calls_hbm": kernel_rates(call_bytes(cfg, counts, cfg.tokens, bool(al.any()),
+                                                bool((al == 0).any())), mean)}
+    del layer, x, bufs
+    torch.cuda.empty_cache()
+    return res
+
+
+def stack_bench(args, dev):
+    """The 48-layer Qwen-shaped stack (16384 tokens in 32 requests of 512, attention
+    replaced by identity, h <- bf16(h + MoE(h)), independent weights per layer, 72.5 GB on
+    the device): one all-allow and one all-deny pass, each timed whole after a warm-up
+    pass, with the summed private-row audit."""
+    import torch
+    import workloads as W
+    import paper_2608_06690_amd as P
+    cfg = W.get_config("stack")
+    L, T = cfg.layers, cfg.tokens
+    desc = P.make_desc(cfg.hidden, cfg.inter, cfg.n_pub, cfg.n_priv, cfg.top_k)
+    layers = []
+    for ell in range(L):
+        Lw = W.make_layer(cfg, ell, dev)
+        layers.append(P.PolicyMaskedMoE(desc, Lw.wr_pub, Lw.wr_priv, Lw.bias, Lw.w13_pub, Lw.w2_pub,
+                                        Lw.w13_priv, Lw.w2_priv))
+    x0 = W.make_x(cfg, dev)
+    bufs = layers[0].buffers(T)
+    stream = torch.cuda.current_stream()
+    flop_layer = T * cfg.top_k * 6 * cfg.hidden * cfg.inter
+    res = {"workload": "48-layer qwen3-30b-a3b-shaped moe stack, 32 requests x 512 tokens",
+           "layers": L, "tokens": T, "flop_per_pass": flop_layer * L}
+    for p, kind in ((0, "allow"), (1, "deny")):
+        req = W.make_requests(cfg, p)
+        words = P.token_policy_words(req.metas, req.lengths, dev)
+        req_off = P.request_offsets(req.lengths, dev)
+        audit = layers[0].audit_buffers(T, cfg.requests)
+
+        def one_pass(events=None):
+            h = x0.clone()
+            audit.zero_()
+            for ell, layer in enumerate(layers):
+                layer.route(h, words, bufs, stream)
+                layer.dispatch(h, bufs, stream)
+                if events:
+                    events[ell][0].record(stream)
+                layer.expert_ffn(h, bufs, audit, stream)
+                if events:
+                    events[ell][1].record(stream)
+                layer.combine(h, bufs, stream)
+                h = (h.float() + bufs.out.float()).to(torch.bfloat16)
+            layers[0].audit(T, bufs, audit, req_off, stream)
+            return h
+
+        one_pass()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        one_pass()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(L)]
+        one_pass(ev)
+        torch.cuda.synchronize()
+        ffn_us = sum(a.elapsed_time(b) for a, b in ev) * 1e3
+        res[kind] = {"pass_ms": wall * 1e3, "layer_tokens_per_s": T * L / wall,
+                     "ffn_us_per_layer": ffn_us / L,
+                     "ffn_tflops": flop_layer * L / (ffn_us * 1e-6) / 1e12,
+                     "ffn_mfma_frac": flop_layer * L / (ffn_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS,
+                     "private_rows_audited": int(audit.total.item()),
+                     "private_rows_expected": L * T * cfg.top_k if kind == "allow" else 0,
+                     "deny_violations": int(audit.violations.item())}
+    del layers, bufs
     torch.cuda.empty_cache()
     return res
 
@@ -497,6 +592,9 @@ def main():
     if args.vendor_gemm:
         print(json.dumps(vendor_gemm_bench(dev)), flush=True)
         return
+    if args.stack_only:
+        print(json.dumps(stack_bench(args, dev)), flush=True)
+        return
     if args.fingerprint_only:
         print(json.dumps(fingerprint_bench(args, dev)), flush=True)
         return
@@ -551,6 +649,10 @@ def main():
 
     if not args.no_decode:
         out["decode"] = decode_bench(args, dev)
+    if not args.no_deepseek:
+        out["deepseek"] = deepseek_bench(args, dev)
+    if args.stack:
+        out["stack"] = stack_bench(args, dev)
     if not args.no_backward:
         out["backward"] = backward_bench(args, dev)
     if not args.no_fingerprint:
