@@ -43,7 +43,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "388292c16f265b3d581b2485720c942a0e778310ae4eaff3161650057b6aa66a": 1_992_933_577,
+    "40febd022281b6381cb33319d6bd42398cac1c2e8fc5bd94b9d27237bddae120": 1_994_457_234,
 }
 
 
