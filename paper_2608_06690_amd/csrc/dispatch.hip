@@ -13,6 +13,9 @@
 //           row = offset + chunk base + rank; token_row[t*k+j] = row; row_token[row] = t.
 //  gather   (optional) one wave per permuted row copies x[row_token[row]] to
 //           x_perm[row] in 16-byte vectors, so reads and writes are coalesced.
+// Small batches (up to 8192 (token, slot) pairs, e.g. decode) whose masks and chunk
+// bases fit in LDS run hist, count and scatter back to back in one workgroup
+// (dispatch_fused_kernel): one launch instead of three, and the same outputs.
 // No order-dependent atomics: the permutation is deterministic. Expert ids outside
 // [0, E) are not counted and get token_row = -1.
 #include "pmpe_internal.h"
@@ -113,6 +116,75 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchAr
   }
 }
 
+constexpr int DF_THREADS = 1024;
+constexpr size_t DF_MAX_LDS = 144 * 1024;  // masks (8 B) and chunk bases (4 B) of every (chunk, expert)
+constexpr int64_t DF_MAX_PAIRS = 8192;      // (token, slot) pairs up to which one workgroup is used
+
+// Single-workgroup dispatch: the same three steps as hist / count / scatter, with the
+// chunk masks and chunk bases in LDS.
+__global__ __launch_bounds__(DF_THREADS) void dispatch_fused_kernel(DispatchArgs a, int nchunks) {
+  __shared__ __attribute__((aligned(16))) unsigned char df_smem[DF_MAX_LDS];
+  __shared__ int s_off[DP_MAX_E + 1];
+  __shared__ int s_wsum[DF_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int E = a.E, k = a.k;
+  const int np = a.T * k;
+  unsigned long long* s_mask = (unsigned long long*)df_smem;  // [nchunks][E]
+  int* s_base = (int*)(df_smem + (size_t)nchunks * E * 8);    // [nchunks][E]
+  for (int i = tid; i < nchunks * E; i += DF_THREADS) s_mask[i] = 0ull;
+  __syncthreads();
+  // hist: bit (token mod 64) of mask[chunk][expert] (64-bit atomic OR, order independent)
+  for (int p = tid; p < np; p += DF_THREADS) {
+    const int e = a.topk_idx[p];
+    const int t = p / k;
+    if (e >= 0 && e < E) atomicOr(&s_mask[(t / DP_TOK) * E + e], 1ull << (t % DP_TOK));
+  }
+  __syncthreads();
+  // count: per expert, its chunks' popcounts in chunk order
+  for (int e = tid; e < E; e += DF_THREADS) {
+    int running = 0;
+    for (int c = 0; c < nchunks; ++c) {
+      s_base[c * E + e] = running;
+      running += popc64(s_mask[c * E + e]);
+    }
+    a.count[e] = running;
+    s_off[e] = running;
+  }
+  __syncthreads();
+  // expert offsets: exclusive scan of the counts
+  int running = 0;
+  for (int e0 = 0; e0 < E; e0 += DF_THREADS) {
+    const int e = e0 + tid;
+    const int v = (e < E) ? s_off[e] : 0;
+    const int incl = wave_incl_scan(v);
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int before = running;
+    for (int w = 0; w < wave; ++w) before += s_wsum[w];
+    int tot = 0;
+    for (int w = 0; w < DF_THREADS / 64; ++w) tot += s_wsum[w];
+    __syncthreads();  // every count of this range is read before the offsets replace them
+    if (e < E) s_off[e] = before + incl - v;
+    running += tot;
+  }
+  __syncthreads();
+  if (tid == 0) s_off[E] = running;
+  __syncthreads();
+  for (int e = tid; e <= E; e += DF_THREADS) a.offset[e] = s_off[e];
+  // scatter: row = offset + chunk base + rank of the token among its chunk's rows of e
+  for (int p = tid; p < np; p += DF_THREADS) {
+    const int e = a.topk_idx[p];
+    int row = -1;
+    if (e >= 0 && e < E) {
+      const int t = p / k, c = t / DP_TOK, tl = t % DP_TOK;
+      const uint64_t below = (tl == 0) ? 0ull : (s_mask[c * E + e] & ((1ull << tl) - 1ull));
+      row = s_off[e] + s_base[c * E + e] + popc64(below);
+      a.row_token[row] = t;
+    }
+    a.token_row[p] = row;
+  }
+}
+
 constexpr int GA_WAVES = 4;
 
 __global__ __launch_bounds__(64 * GA_WAVES) void gather_rows_kernel(DispatchArgs a, int nrows) {
@@ -134,9 +206,16 @@ int dispatch_chunks(int T) { return (T + DP_TOK - 1) / DP_TOK; }
 
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
   const int nchunks = dispatch_chunks(a.T);
-  hipLaunchKernelGGL(dispatch_hist_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
-  hipLaunchKernelGGL(dispatch_count_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
-  hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
+  const size_t fused_lds = (size_t)nchunks * a.E * 12;
+  // one workgroup is faster only while the pairs are few (measured: 256 x 8 pairs 12.6 -> 8 us;
+  // 4096 x 8 pairs 13 -> 36 us)
+  if (fused_lds <= DF_MAX_LDS && (int64_t)a.T * a.k <= DF_MAX_PAIRS) {
+    hipLaunchKernelGGL(dispatch_fused_kernel, dim3(1), dim3(DF_THREADS), 0, s, a, nchunks);
+  } else {
+    hipLaunchKernelGGL(dispatch_hist_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
+    hipLaunchKernelGGL(dispatch_count_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
+    hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
+  }
   if (a.x_perm) {
     const int nrows = a.T * a.k;
     hipLaunchKernelGGL(gather_rows_kernel, dim3((nrows + GA_WAVES - 1) / GA_WAVES),
