@@ -652,7 +652,24 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
   e = launch_gemm<false, true, false, EPI_F32>(g, mt_max * (g.N / TN), s);
   if (e != hipSuccess) return e;
   }
-  if (a.n_priv > 0) {
+  if (a.n_priv > 0 && a.tr) {
+    // K-contiguous copies of the private rows (zero-padded per expert to multiples of 64),
+    // then the weight gradients on MFMA with 256 x 256 tiles; the copies of one product
+    // are dead once it has run, so the next product reuses the region
+    // dW2[p] = dY^T Hh over private expert p's rows: M = H, N = I
+    uint16_t* at = a.tr;
+    uint16_t* bt = a.tr + (size_t)H * a.P;
+    e = launch_transpose_priv(a.dY, at, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    if (e == hipSuccess) e = launch_transpose_priv(a.Hh, bt, R, I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    if (e == hipSuccess) e = launch_wgrad(WgradArgs{H, I, a.P, a.n_pub, a.n_priv, at, bt, a.count, a.dw2_priv}, s);
+    if (e != hipSuccess) return e;
+    // dW13[p] = [da; db]^T Xp: M = 2I, N = H
+    bt = a.tr + (size_t)2 * I * a.P;
+    e = launch_transpose_priv(a.dA13, at, R, 2 * I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    if (e == hipSuccess) e = launch_transpose_priv(a.Xp, bt, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    if (e == hipSuccess) e = launch_wgrad(WgradArgs{2 * I, H, a.P, a.n_pub, a.n_priv, at, bt, a.count, a.dw13_priv}, s);
+    if (e != hipSuccess) return e;
+  } else if (a.n_priv > 0) {
     // dW2[p] = dY^T Hh over private expert p's rows: M = H, N = I
     GemmArgs w{};
     w.count = a.count; w.offset = a.offset; w.n_pub = a.n_pub;
@@ -666,6 +683,8 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     w.C = a.dw13_priv; w.ldc = H; w.strideC = (size_t)2 * I * H; w.M = 2 * I; w.N = H;
     e = launch_gemm<true, true, true, EPI_F32>(w, a.n_priv * (2 * I / TM) * (H / TN), s);
     if (e != hipSuccess) return e;
+  }
+  if (a.n_priv > 0) {
     if (a.pool_gates)
       bwd_dwr_pool_part_kernel<<<dim3(a.n_priv, BWD_DWR_SPLIT), BT, 0, s>>>(a);
     else

@@ -616,6 +616,114 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Private-expert weight gradients: C[p] [M, N] = AT_p BT_p^T, K = private expert p's rows
+// (padded to a multiple of 64 with zero rows), AT [M, P] and BT [N, P] K-contiguous. One
+// block per (expert, N tile, M tile), consecutive indices on one XCD; the same 256 x 256 x 64
+// tile, two-stage global->LDS copy ring, swizzle and MFMA fragments as the forward's
+// prefill GEMM, fp32 results stored from the accumulators. An expert without rows gets
+// zeros. The K order of every output element is fixed, so the result is deterministic.
+// ---------------------------------------------------------------------------
+template <class C>
+__global__ __launch_bounds__(C::THREADS) void wgrad_kernel(WgradArgs a) {
+  static_assert(C::STAGES == 2 && !C::W8 && C::BK == 64, "two stages of bf16 K steps of 64");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
+  __shared__ int s_k[2];
+  constexpr int BK = C::BK, NB = C::BN / C::WN / 16, MB = C::MB, WCOLS = C::BN / C::WN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int uwave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = uwave / C::WN, wn = uwave % C::WN;
+  const int mtiles = (a.M + C::BM - 1) / C::BM, ntiles = (a.N + C::BN - 1) / C::BN;
+  const int total = a.n_priv * ntiles * mtiles;
+  const int per = (int)gridDim.x >> 3;  // the grid is a multiple of 8
+  const int L = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (L >= total) return;
+  const int pe = L / (ntiles * mtiles), rem = L - pe * (ntiles * mtiles);
+  const int nt = rem / mtiles, mt = rem - nt * mtiles;
+  if (tid < 64) {  // padded offset and padded row count of expert pe
+    int running = 0;
+    for (int q0 = 0; q0 < pe; q0 += 64) {
+      const int q = q0 + tid;
+      running += wave_sum_int(q < pe ? (a.count[a.n_pub + q] + 63) / 64 * 64 : 0);
+    }
+    if (tid == 0) {
+      s_k[0] = running;
+      s_k[1] = (a.count[a.n_pub + pe] + 63) / 64 * 64;
+    }
+  }
+  __syncthreads();
+  const int po = s_k[0], nk = s_k[1] / BK;
+  const int m0 = mt * C::BM, n0 = nt * C::BN;
+  const int lrow = lane / C::CH, lphys = lane % C::CH;
+  uint32_t offA[C::A_DMA], offB[C::B_DMA];
+#pragma unroll
+  for (int i = 0; i < C::A_DMA; ++i) {
+    const int r = (uwave * C::A_DMA + i) * C::RPD + lrow;
+    const int m = min(m0 + r, a.M - 1);  // rows past M reload row M-1 (never stored)
+    offA[i] = ((uint32_t)m * (uint32_t)a.P + (uint32_t)po + (uint32_t)((lphys ^ (r & 7)) * 8)) * 2;
+  }
+#pragma unroll
+  for (int i = 0; i < C::B_DMA; ++i) {
+    const int r = (uwave * C::B_DMA + i) * C::RPD + lrow;
+    const int n = min(n0 + r, a.N - 1);
+    offB[i] = ((uint32_t)n * (uint32_t)a.P + (uint32_t)po + (uint32_t)((lphys ^ (r & 7)) * 8)) * 2;
+  }
+  const uint32_t lds0 = lds_addr(smem);
+  auto issue = [&](int slot, int k0) {
+    const uint32_t sa = __builtin_amdgcn_readfirstlane(lds0 + slot * C::STAGE);
+    const uint32_t wa = sa + uwave * C::A_DMA * 1024, wb = sa + C::A_BYTES + uwave * C::B_DMA * 1024;
+    const uint16_t* ba = a.AT + k0;
+    const uint16_t* bb = a.BT + k0;
+    Unroll<0, C::A_DMA>::run([&](auto i) { dma16s<i.value * 1024, false>(offA[i.value], ba, wa); });
+    Unroll<0, C::B_DMA>::run([&](auto i) { dma16s<i.value * 1024, false>(offB[i.value], bb, wb); });
+  };
+  f32x4 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0, 0, 0, 0};
+  uint32_t lane_off[BK / 32];
+#pragma unroll
+  for (int sub = 0; sub < BK / 32; ++sub) lane_off[sub] = (uint32_t)swz<BK>(lane & 15, sub * 4 + (lane >> 4));
+  if (nk > 0) issue(0, 0);
+  for (int kc = 0; kc < nk; ++kc) {
+    wait_vmcnt<0>();  // this wave's copies of step kc landed ...
+    barrier_raw();    // ... and every wave's; every read of step kc-1 is finished
+    if (kc + 1 < nk) issue((kc + 1) & 1, (kc + 1) * BK);
+    const int slot = kc & 1;
+#pragma unroll
+    for (int sub = 0; sub < BK / 32; ++sub) {
+      bf16x8 fa[MB], fb[NB];
+      const uint32_t pa = lane_off[sub] + slot * C::STAGE + wm * 16 * C::RB;
+      const uint32_t pb = lane_off[sub] + slot * C::STAGE + C::A_BYTES + wn * WCOLS * C::RB;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) fb[nb] = as_bf16x8(*(const u32x4*)(smem + pb + nb * 16 * C::RB));
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) fa[mb] = as_bf16x8(*(const u32x4*)(smem + pa + mb * C::WM * 16 * C::RB));
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // lane holds C[m = 4 (lane / 16) + i][n = lane % 16] of each 16 x 16 block
+  float* cp = a.C + (size_t)pe * a.M * a.N;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + (mb * C::WM + wm) * 16 + (lane >> 4) * 4 + i;
+      if (m >= a.M) continue;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int n = n0 + wn * WCOLS + nb * 16 + (lane & 15);
+        if (n < a.N) cp[(size_t)m * a.N + n] = acc[mb][nb][i];
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // fp32 path support: tile of F32_BM rows of one expert (same device-side lookup)
 // ---------------------------------------------------------------------------
 constexpr int F32_BM = 128;
@@ -795,6 +903,14 @@ hipError_t launch_expert_ffn_fp8(const FfnArgs& a, hipStream_t s) {
     run(CfgLarge8{});
   else
     run(CfgSmall8{});
+  return hipGetLastError();
+}
+
+hipError_t launch_wgrad(const WgradArgs& a, hipStream_t s) {
+  using C = Cfg<256, 256, 4, 2, 2, 64>;
+  const int64_t total = (int64_t)a.n_priv * ((a.M + C::BM - 1) / C::BM) * ((a.N + C::BN - 1) / C::BN);
+  if (total == 0) return hipSuccess;
+  hipLaunchKernelGGL(wgrad_kernel<C>, dim3((unsigned)((total + 7) / 8 * 8)), dim3(C::THREADS), 0, s, a);
   return hipGetLastError();
 }
 

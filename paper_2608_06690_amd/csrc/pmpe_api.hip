@@ -75,7 +75,8 @@ pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR
 
 // backward workspace: Xp, dY, [a; b], h, [da; db], row input gradients, row dz
 struct BwdLayout {
-  size_t xp, dy, ab, hh, da, dxr, dz, part, dzp, absh, dash, dxsh, dh, total;
+  size_t xp, dy, ab, hh, da, dxr, dz, part, dzp, absh, dash, dxsh, dh, tr, total;
+  int P;  // row stride of the transposed private rows (0: weight gradients on the transposing GEMM)
 };
 int bwd_pool_stride(const pmpe_layer_desc* d) {
   if (d->route_mode == PMPE_ROUTE_SOFT) return d->n_pub + d->n_priv;
@@ -99,6 +100,16 @@ BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
   L.dash = o; o += round_up(Tt * 2 * Is * 2);
   L.dxsh = o; o += Is > 0 ? round_up(Tt * H * 4) : 0;
   L.dh = o; o += round_up(R * I * 2);
+  // private rows transposed and padded per expert: [max(2I + H, H + I), P] bf16, used when
+  // every byte offset of the weight-gradient copies fits in 31 bits
+  const size_t P = (R + 63) / 64 * 64 + 64 * (size_t)d->n_priv;
+  const size_t wmax = 2 * I > H ? 2 * I : H;
+  L.P = 0;
+  L.tr = o;
+  if (d->n_priv > 0 && wmax * P * 2 < ((size_t)1 << 31)) {
+    L.P = (int)P;
+    o += round_up((2 * I + H) * P * 2);
+  }
   L.total = o;
   return L;
 }
@@ -449,7 +460,8 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
             d->n_shared > 0 ? d->n_shared * d->shared_inter : 0, w13_sh, w2_sh,
             (float*)(w + L.absh), (uint16_t*)(w + L.dash),
             d->n_shared > 0 ? (float*)(w + L.dxsh) : nullptr,
-            any_t ? w2t_pub : nullptr, w13t_pub, w2t_priv, w13t_priv, (uint16_t*)(w + L.dh)};
+            any_t ? w2t_pub : nullptr, w13t_pub, w2t_priv, w13t_priv, (uint16_t*)(w + L.dh),
+            L.P > 0 ? (uint16_t*)(w + L.tr) : nullptr, L.P};
   return launched(launch_backward(a, (hipStream_t)stream));
 }
 

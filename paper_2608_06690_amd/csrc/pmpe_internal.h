@@ -48,6 +48,12 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
 __device__ __forceinline__ int wave_incl_scan(int v) {
   const int lane = lane_id();
 #pragma unroll
@@ -253,11 +259,30 @@ struct BwdArgs {
   const void* w2t_priv;
   const void* w13t_priv;
   uint16_t* dH;           // [T*k, I] bf16 (NT path)
+  // private rows transposed and padded per expert ([max(2I + H, H + I), P] bf16), or NULL:
+  // the weight gradients then run on the transposing GEMM
+  uint16_t* tr;
+  int P;
 };
 constexpr int BWD_DWR_SPLIT = 16;  // row chunks per private expert in the router-row gradient
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t s);
 hipError_t launch_transpose(const void* src, void* dst, int n, int rows, int cols, hipStream_t s);
+hipError_t launch_transpose_priv(const void* src, void* dst, int rows_max, int cols, int P,
+                                 const int32_t* count, const int32_t* offset, int n_pub,
+                                 int n_priv, hipStream_t s);
+
+// Weight gradients of the private experts on MFMA from K-contiguous operands:
+// C[p] [M, N] fp32 = sum over the padded rows j of private expert p of AT[m][po_p + j] *
+// BT[n][po_p + j], with AT [M, P] and BT [N, P] from launch_transpose_priv.
+struct WgradArgs {
+  int M, N, P, n_pub, n_priv;
+  const uint16_t* AT;
+  const uint16_t* BT;
+  const int32_t* count;
+  float* C;
+};
+hipError_t launch_wgrad(const WgradArgs& a, hipStream_t s);
 
 // Fingerprint tree: 1 KiB leaves, 16 digests per inner node.
 constexpr uint32_t kFpLeafBytes = 1024;
