@@ -1,41 +1,53 @@
 // Per-expert transposes of bf16 weight matrices: dst[e] = src[e]^T for n matrices of
 // [rows, cols]. The backward multiplies by W2 and W13 along their output dimension; with
 // transposed copies (K contiguous) those products run on the same grouped NT GEMM as the
-// forward. 64 x 64 tiles staged through LDS (rows padded by two elements), 8-byte loads
-// and stores along the contiguous dimension on both sides.
+// forward. 64 x 64 tiles staged through LDS, 16-byte loads and stores along the
+// contiguous dimension on both sides.
 #include "pmpe_internal.h"
 
 namespace pmpe {
 namespace {
 
 constexpr int TT = 64;
+constexpr int TP = TT + 8;  // LDS row pitch in elements (144 bytes: 16-byte aligned rows)
+
+// One 64 x 64 tile: rows r of the source (row_ptr(r) or nullptr for a zero row, 16-byte
+// aligned) to dst rows c, dst[c * ld_dst + r]. 16-byte loads and stores on both sides;
+// the LDS tile is written in 16-byte rows and read down its columns.
+template <class RowPtr>
+__device__ __forceinline__ void tile_transpose(RowPtr row_ptr, uint16_t* __restrict__ dst,
+                                               size_t ld_dst) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[TT][TP];
+  const int tid = threadIdx.x;
+  const int q = tid & 7;  // 16-byte chunk
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = (tid >> 3) + 32 * i;
+    const uint16_t* src = row_ptr(r);
+    const u32x4 v = src ? *(const u32x4*)(src + q * 8) : u32x4{0, 0, 0, 0};
+    *(u32x4*)&tile[r][q * 8] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = (tid >> 3) + 32 * i;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      w[e] = (uint32_t)tile[q * 8 + 2 * e][c] | ((uint32_t)tile[q * 8 + 2 * e + 1][c] << 16);
+    *(u32x4*)(dst + (size_t)c * ld_dst + q * 8) = u32x4{w[0], w[1], w[2], w[3]};
+  }
+}
 
 __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restrict__ src,
                                                          uint16_t* __restrict__ dst, int rows,
                                                          int cols) {
-  __shared__ uint16_t tile[TT][TT + 2];
   const size_t mat = (size_t)rows * cols;
   const uint16_t* s = src + (size_t)blockIdx.z * mat;
   uint16_t* d = dst + (size_t)blockIdx.z * mat;
   const int r0 = blockIdx.y * TT, c0 = blockIdx.x * TT;
-  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
-  typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = ty + 16 * i;
-    const u16x4 v = *(const u16x4*)(s + (size_t)(r0 + r) * cols + c0 + tx * 4);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) tile[r][tx * 4 + j] = v[j];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = ty + 16 * i;  // row of dst = column of src
-    u16x4 v;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = tile[tx * 4 + j][c];
-    *(u16x4*)(d + (size_t)(c0 + c) * rows + r0 + tx * 4) = v;
-  }
+  tile_transpose([&](int r) { return s + (size_t)(r0 + r) * cols + c0; }, d + (size_t)c0 * rows + r0,
+                 (size_t)rows);
 }
 
 // Private rows, transposed and padded: src [rows, cols] holds the permuted rows; private
@@ -48,7 +60,6 @@ __global__ __launch_bounds__(256) void transpose_priv_kernel(const uint16_t* __r
                                                               int P, const int32_t* count,
                                                               const int32_t* offset, int n_pub,
                                                               int n_priv) {
-  __shared__ uint16_t tile[TT][TT + 2];
   __shared__ int s_po[PMPE_MAX_POOL + 1];
   const int tid = threadIdx.x;
   if (tid < 64) {
@@ -75,25 +86,9 @@ __global__ __launch_bounds__(256) void transpose_priv_kernel(const uint16_t* __r
   const int cnt = count[n_pub + pp];
   const int src0 = offset[n_pub + pp] + jl;
   const int c0 = blockIdx.y * TT;
-  const int ty = tid >> 4, tx = tid & 15;
-  typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = ty + 16 * i;
-    u16x4 v = u16x4{0, 0, 0, 0};
-    if (jl + r < cnt) v = *(const u16x4*)(src + (size_t)(src0 + r) * cols + c0 + tx * 4);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) tile[r][tx * 4 + j] = v[j];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = ty + 16 * i;
-    u16x4 v;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = tile[tx * 4 + j][c];
-    *(u16x4*)(dst + (size_t)(c0 + c) * P + j0 + tx * 4) = v;
-  }
+  tile_transpose([&](int r) -> const uint16_t* {
+    return (jl + r < cnt) ? src + (size_t)(src0 + r) * cols + c0 : nullptr;
+  }, dst + (size_t)c0 * P + j0, (size_t)P);
 }
 
 }  // namespace
