@@ -43,7 +43,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "40febd022281b6381cb33319d6bd42398cac1c2e8fc5bd94b9d27237bddae120": 1_994_457_234,
+    "2cff456db010eb00a53100718d673c4b09ddddd0bf8d00a3a441f08c4298bc3b": 2_022_751_287,
 }
 
 
