@@ -43,7 +43,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "2cff456db010eb00a53100718d673c4b09ddddd0bf8d00a3a441f08c4298bc3b": 2_022_751_287,
+    "d3683543e3e1083596bb166b769dea0c13abb6c60f867c53779ad6744da7f38b": 2_008_443_886,
 }
 
 

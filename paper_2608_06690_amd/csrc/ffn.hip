@@ -29,86 +29,11 @@
 // whole 16-byte vectors.
 #include <type_traits>
 
+#include "lds_dma.h"
 #include "pmpe_internal.h"
 
 namespace pmpe {
 namespace {
-
-typedef __attribute__((address_space(3))) unsigned char lds_u8;
-
-// 32-bit LDS address of a shared-memory pointer.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const lds_u8*)p;
-}
-
-// Global -> LDS copy of 16 bytes per lane: lane l's bytes land at lds_base + 16 * l
-// (lds_base is wave-uniform, held in M0). Written as inline assembly so that the
-// compiler does not treat the copy as a pending LDS write that every later LDS read
-// must wait for; the kernel waits for its own copies explicitly (wait_vmcnt) before
-// a barrier and only then reads the stage they filled.
-__device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
-  asm volatile(
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off" ::"v"(src),
-      "s"(lds_base)
-      : "memory", "m0");
-}
-// Same copy addressed as a wave-uniform 64-bit base (SGPRs) plus a per-lane 32-bit
-// byte offset; the LDS destination is a wave-uniform base plus the immediate IMM.
-// The base and the LDS address must be wave-uniform; they are passed through
-// readfirstlane so that they are held in SGPRs whatever the compiler can prove.
-__device__ __forceinline__ const void* uniform_ptr(const void* p) {
-  const uint64_t v = (uint64_t)(uintptr_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
-}
-// NT: non-temporal hint, for operands that are read once (streamed weights).
-template <int IMM, bool NT>
-__device__ __forceinline__ void dma16s(uint32_t byte_off, const void* base_, uint32_t lds_base_) {
-  const void* base = uniform_ptr(base_);
-  const uint32_t lds_base = __builtin_amdgcn_readfirstlane(lds_base_);
-  if constexpr (NT)
-    asm volatile(
-        "s_add_u32 m0, %2, %3\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %0, %1 offset:0 nt" ::"v"(byte_off),
-        "s"(base), "s"(lds_base), "n"(IMM)
-        : "memory", "m0");
-  else
-    asm volatile(
-        "s_add_u32 m0, %2, %3\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %0, %1 offset:0" ::"v"(byte_off),
-        "s"(base), "s"(lds_base), "n"(IMM)
-        : "memory", "m0");
-}
-
-template <int I, int N>
-struct Unroll {
-  template <class F>
-  __device__ __forceinline__ static void run(F&& f) {
-    f(std::integral_constant<int, I>{});
-    Unroll<I + 1, N>::run(f);
-  }
-};
-template <int N>
-struct Unroll<N, N> {
-  template <class F>
-  __device__ __forceinline__ static void run(F&&) {}
-};
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Workgroup barrier without the full memory drain that __syncthreads() implies: the
-// copies a stage depends on were already waited for (wait_vmcnt), and every LDS read
-// of the previous stage was consumed by an MFMA before this point. Later stages'
-// copies stay in flight across it.
-__device__ __forceinline__ void barrier_raw() { asm volatile("s_barrier" ::: "memory"); }
 
 // LDS operand tiles hold BK bf16 per row (RB = 2*BK bytes, CH = BK/8 chunks of 16
 // bytes). Chunk c of row r is stored at chunk c ^ f(r): f(r) = r & 7 for 128-byte

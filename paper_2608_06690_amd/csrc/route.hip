@@ -1,12 +1,15 @@
 // K1 - fused policy-masked router (Sec. 3.1 mask equation; App. B.1).
 //
-// One workgroup of 8 waves routes a tile of 32 tokens:
+// A logits kernel over (token tile, 16-expert group of one pool) blocks, then a top-k
+// kernel with one wave per token:
 //  1. Decode each token's policy word: tau = (word == PMPE_POLICY_ALLOW); a NULL word
 //     array, a malformed word or a missing private router all give deny.
-//  2. Logits over the permitted pool only. For the public pass, rows of allow tokens are
-//     fed as zeros and their results discarded; for the private pass the same holds for
-//     deny tokens, so a deny token's x is never multiplied with a private router row,
-//     and a pass with no token of its policy is skipped (its router rows are not read).
+//  2. Logits over the permitted pool only. A block feeds only the tokens whose policy
+//     selects its pool: other rows load a token of this pool's policy and their results
+//     are discarded, so a deny token's x is never multiplied with a private router row,
+//     and a block with no token of its policy returns before reading its router rows.
+//     Up to 2048 tokens the operands are loaded straight into registers (16-token tiles,
+//     H split across the four waves); larger batches stage them in LDS (64-token tiles).
 //     bf16 activations: the fp32 router row w is split exactly into three bf16 parts
 //     w = hi + mid + lo (each truncation keeps the next 8 significant bits, so the sum
 //     is exact for normal w); every product x * part is exact in fp32 and the MFMA
@@ -17,6 +20,7 @@
 //     going to the lower id (-0.0 == +0.0, NaN ranks as -inf).
 //  4. Gates (RENORM over the k winners, or POOL_SOFTMAX over the whole pool) in fp32,
 //     written in ascending expert-id order; kgap = z_(k) - z_(k+1).
+#include "lds_dma.h"
 #include "pmpe_internal.h"
 
 namespace pmpe {
@@ -280,6 +284,173 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   }
 }
 
+// Large batches: token-tile x expert-group logits with both operands staged in LDS.
+// Block (tile, g): 64 tokens against RL_NE experts of one pool; wave w owns the tile's
+// 16-token row block w over the whole of H, so no partial sums are exchanged. K steps of
+// 64: a step's x rows (64 x 128 bytes) and fp32 router rows (RL_NE x 256 bytes) are copied
+// whole into a ring of RL_D stages by global->LDS copies, so every request is a full
+// 128-byte line (loads of 64-byte row pieces straight into the MFMA register layout
+// bound the register kernel at this size). The 16-byte chunks of each LDS row are
+// XOR-swizzled by row so that the fragment reads of 16 rows hit distinct banks. Token
+// selection, the exact three-part split, the pool rule and the K rotation are those of
+// the register kernel.
+// 16 experts per block and 6 stages (72 KiB, two blocks per CU): the kernel is bound by the
+// copies in flight per CU, so more concurrent blocks beat fewer re-reads (Qwen-shaped
+// 4096-token batch: 32 experts per block 43 us, 16 experts with 4 stages 38 us, with 6
+// stages 35 us, the register kernel 46 us, top-k included).
+constexpr int RL_TT = 64, RL_NE = 16, RL_BK = 64, RL_D = 6;
+constexpr int RL_NB = RL_NE / 16;            // 16-expert blocks per wave
+constexpr int RL_XB = RL_TT * RL_BK * 2;     // x bytes per stage (8 KiB)
+constexpr int RL_WB = RL_NE * RL_BK * 4;     // router bytes per stage
+constexpr int RL_STAGE = RL_XB + RL_WB;
+constexpr int RL_WDMA = RL_WB / 1024 / 4;    // router copies per wave per stage (4 rows each)
+constexpr int RL_NDMA = 2 + RL_WDMA;         // copies per wave per stage: 2 of x, the router's
+static_assert(RL_NE % 16 == 0 && RL_WDMA >= 1, "router tile");
+
+// Wait for the copies of the oldest step in flight: `younger` steps were issued after it
+// (RL_NDMA copies each, loads complete in order), at most Y of which may stay in flight.
+template <int Y>
+__device__ __forceinline__ void wait_steps(int younger) {
+  if constexpr (Y == 0)
+    wait_vmcnt<0>();
+  else if (younger >= Y)
+    wait_vmcnt<Y * RL_NDMA>();
+  else
+    wait_steps<Y - 1>(younger);
+}
+
+__global__ __launch_bounds__(RT_THREADS) void route_logits_lds_kernel(RouteArgs a, int ntiles, int ngroups) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[RL_D * RL_STAGE];
+  __shared__ int s_tau[RL_TT];
+  __shared__ int s_first;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // 1-D grid, (token tile, expert group) with the group fastest, XCD-contiguous
+  const int total = ntiles * ngroups;
+  const int b = blockIdx.x, xcd = b & 7, j = b >> 3;
+  const int cnt_x = (total >> 3) + (xcd < (total & 7) ? 1 : 0);
+  if (j >= cnt_x) return;
+  const int L = xcd * (total >> 3) + min(xcd, total & 7) + j;
+  const int tile = L / ngroups, grp = L - tile * ngroups;
+  const int t0 = tile * RL_TT;
+  const int gpub = (a.n_pub + RL_NE - 1) / RL_NE;
+  const int pass = grp < gpub ? 0 : 1;
+  const int n0 = (pass ? grp - gpub : grp) * RL_NE;
+  const int N = pass ? a.n_priv : a.n_pub;
+  if (tid == 0) s_first = RL_TT;
+  __syncthreads();
+  int mine = 0;
+  if (tid < RL_TT) {
+    const int tau = (t0 + tid < a.T) ? token_tau(a, t0 + tid) : -1;
+    s_tau[tid] = tau;
+    mine = (a.soft ? tau >= 0 : tau == pass) ? 1 : 0;
+    if (mine) atomicMin(&s_first, tid);
+  }
+  // no token of this pool's policy in the tile: its router rows are never read
+  if (!__syncthreads_or(mine)) return;
+  const int H = a.H;
+  const int first = s_first;
+  auto part = [&](int r) { return a.soft ? s_tau[r] >= 0 : s_tau[r] == pass; };
+  // Copy sources, byte offsets from the step's base. x: copy jj of wave w fills LDS rows
+  // (2w + jj) * 8 + l / 8, lane l's physical chunk l % 8 holding logical chunk
+  // (l % 8) ^ ((row >> 1) & 7); a row whose token has the other policy (or lies past T)
+  // copies the tile's first token of this policy, so a token's x is only ever read for
+  // the pool it is permitted. Router: copy jj of wave w fills rows (RL_WDMA w + jj) * 4 +
+  // l / 16, physical chunk l % 16 holding logical chunk (l % 16) ^ (row & 15); rows past
+  // the pool copy expert n0 (their results are discarded).
+  uint32_t offx[2];
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj) {
+    const int r = (2 * wave + jj) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((r >> 1) & 7);
+    const int tok = t0 + (part(r) ? r : first);
+    offx[jj] = ((uint32_t)tok * (uint32_t)H + c * 8) * 2;
+  }
+  uint32_t offw[RL_WDMA];
+#pragma unroll
+  for (int jj = 0; jj < RL_WDMA; ++jj) {
+    const int r = (RL_WDMA * wave + jj) * 4 + (lane >> 4);
+    const int c = (lane & 15) ^ (r & 15);
+    const int n = n0 + r;
+    offw[jj] = ((uint32_t)(n < N ? n : n0) * (uint32_t)H + c * 4) * 4;
+  }
+  const uint16_t* x = (const uint16_t*)a.x;
+  const float* wr = pass ? a.wr_priv : a.wr_pub;
+  const int nsteps = H / RL_BK;
+  const int rot = (tile * 5 + grp * 3) % nsteps;  // concurrent blocks read different columns
+  const uint32_t lds0 = lds_addr(smem);
+  auto issue = [&](int st) {
+    const int kk = ((st + rot) % nsteps) * RL_BK;
+    const uint32_t sx = __builtin_amdgcn_readfirstlane(lds0 + (st % RL_D) * RL_STAGE);
+    dma16s<0, false>(offx[0], x + kk, sx + 2 * wave * 1024);
+    dma16s<1024, false>(offx[1], x + kk, sx + 2 * wave * 1024);
+    const uint32_t sw = sx + RL_XB + RL_WDMA * wave * 1024;
+    Unroll<0, RL_WDMA>::run([&](auto jj) { dma16s<jj.value * 1024, false>(offw[jj.value], wr + kk, sw); });
+  };
+  // Fragment addresses within a stage. A: row 16w + (l & 15), 8 bf16 of K sub-step sub at
+  // logical chunk 4 sub + l / 16. Router block nb: row 16 nb + (l & 15), the same 8 K
+  // values as two fp32 chunks 8 sub + 2 (l / 16) and the next.
+  const int ar = wave * 16 + (lane & 15), nr = lane & 15, g = lane >> 4;
+  uint32_t pa[2], pw[RL_NB][2][2];
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    pa[sub] = ar * 128 + (((sub * 4 + g) ^ ((ar >> 1) & 7)) << 4);
+#pragma unroll
+    for (int nb = 0; nb < RL_NB; ++nb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        pw[nb][sub][h] = RL_XB + (nb * 16 + nr) * 256 + (((sub * 8 + 2 * g + h) ^ nr) << 4);
+  }
+  f32x4 acc[RL_NB];
+#pragma unroll
+  for (int nb = 0; nb < RL_NB; ++nb) acc[nb] = f32x4{0, 0, 0, 0};
+  int issued = 0;
+  for (; issued < RL_D - 1 && issued < nsteps; ++issued) issue(issued);
+  for (int s = 0; s < nsteps; ++s) {
+    // this wave's copies of step s landed (younger steps may stay in flight) ...
+    wait_steps<RL_D - 2>(issued - 1 - s);
+    // ... and every other wave's; every read of step s - 1 is finished
+    barrier_raw();
+    if (issued < nsteps) issue(issued++);  // into the slot of step s - 1
+    const uint32_t st = (uint32_t)(s % RL_D) * RL_STAGE;
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const bf16x8 av8 = as_bf16x8(*(const u32x4*)(smem + st + pa[sub]));
+#pragma unroll
+      for (int nb = 0; nb < RL_NB; ++nb) {
+        const float4 w0 = *(const float4*)(smem + st + pw[nb][sub][0]);
+        const float4 w1 = *(const float4*)(smem + st + pw[nb][sub][1]);
+        const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        uint32_t ph[8], pm[8], pl[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
+        const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
+                                          ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
+        const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
+                                          pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
+        const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
+                                          pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[nb], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's reads of the slot are done
+  }
+  // lane l holds tokens 16w + 4 (l / 16) + i against experts n0 + 16 nb + (l & 15)
+#pragma unroll
+  for (int nb = 0; nb < RL_NB; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tt = wave * 16 + g * 4 + i;
+      const int nn = n0 + nb * 16 + nr;
+      if (!part(tt) || nn >= N) continue;
+      float z = acc[nb][i];
+      if (a.bias) z += a.bias[(pass ? a.n_pub : 0) + nn];
+      a.z[(size_t)(t0 + tt) * a.zstride + (a.soft && pass ? a.n_pub : 0) + nn] = z;
+    }
+}
+
 // fp32 activations (small layers): one thread per (token, expert) pair, fp32 dot
 // products in blocks of 64 terms.
 __global__ __launch_bounds__(RT_THREADS) void route_logits_f32_kernel(RouteArgs a) {
@@ -328,7 +499,12 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   if (a.act_bf16) {
     const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
-    if (a.T > 2048) {
+    // the LDS kernel addresses x with 32-bit byte offsets from the step's base
+    if (a.T > 2048 && (uint64_t)a.T * a.H * 2 < (1ull << 32)) {
+      const int nt = (a.T + RL_TT - 1) / RL_TT;
+      const int lgroups = (a.n_pub + RL_NE - 1) / RL_NE + (a.n_priv + RL_NE - 1) / RL_NE;
+      hipLaunchKernelGGL(route_logits_lds_kernel, dim3((nt * lgroups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, lgroups);
+    } else if (a.T > 2048) {
       const int nt = (a.T + 31) / 32;
       hipLaunchKernelGGL(route_logits_bf16_kernel<32>, dim3((nt * groups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, groups);
     } else {

@@ -98,6 +98,27 @@ def test_small_bf16_layer(shape, gather):
     full_check(cfg, layer, x, words, req)
 
 
+# Batches above 2048 tokens take the router whose operands are staged in LDS (64-token
+# tiles): a ragged last tile, tiles that mix allow and deny tokens (request boundaries off
+# the 64-token grid), pools that are not multiples of 16, and H = 384 (6 K steps, so the
+# per-block K rotation wraps at an odd count).
+LARGE_ROUTE = [
+    dict(tokens=2113, requests=9, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),
+    dict(tokens=4100, requests=5, hidden=384, inter=128, n_pub=128, n_priv=32, top_k=8),
+]
+
+
+@pytest.mark.parametrize("shape", LARGE_ROUTE, ids=lambda s: f"T{s['tokens']}_H{s['hidden']}_E{s['n_pub']}+{s['n_priv']}")
+def test_large_batch_router(shape):
+    cfg = W.scaled_config(W.get_config("qwen"), **shape)
+    layer, _ = C.device_layer(cfg)
+    x = W.make_x(cfg, "cuda")
+    req = W.alternating_requests(cfg.requests, cfg.tokens // cfg.requests)
+    req.lengths[-1] += cfg.tokens - sum(req.lengths)
+    words = O.compile_words(req.metas, req.lengths)
+    full_check(cfg, layer, x, words, req)
+
+
 def test_small_deepseek_like_shared_and_pool_softmax():
     cfg = W.scaled_config(W.get_config("deepseek"), tokens=400, requests=4, hidden=256, inter=128,
                           n_pub=32, n_priv=8, top_k=6, shared_inter=192)

@@ -64,7 +64,9 @@ def test_soft_router_tiny_fp32():
 @pytest.mark.parametrize("shape", [
     dict(tokens=300, requests=6, hidden=256, inter=192, n_pub=24, n_priv=12, top_k=4),
     dict(tokens=200, requests=4, hidden=256, inter=128, n_pub=200, n_priv=100, top_k=8),  # pool of 300
-], ids=["E36", "E300"])
+    # above 2048 tokens: the LDS-staged router, a ragged last tile, mixed-policy tiles
+    dict(tokens=2150, requests=5, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),
+], ids=["E36", "E300", "T2150"])
 def test_soft_router_small_bf16_leaks_and_is_audited(shape):
     cfg = W.scaled_config(W.get_config("qwen"), **shape)
     req = W.alternating_requests(cfg.requests, cfg.tokens // cfg.requests)
