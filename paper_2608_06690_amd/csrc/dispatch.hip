@@ -11,6 +11,8 @@
 //           (each chunk's first row within the expert).
 //  scatter  one workgroup per chunk: expert_offset is the exclusive scan of the counts;
 //           row = offset + chunk base + rank; token_row[t*k+j] = row; row_token[row] = t.
+//           Up to 128 chunks every scatter block recounts the masks of all chunks itself
+//           (dispatch_count_scatter_kernel), so count needs no launch of its own.
 //  gather   (optional) one wave per permuted row copies x[row_token[row]] to
 //           x_perm[row] in 16-byte vectors, so reads and writes are coalesced.
 // Small batches (up to 8192 (token, slot) pairs, e.g. decode) whose masks and chunk
@@ -116,6 +118,69 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchAr
   }
 }
 
+constexpr int DC_MAX_CHUNKS = 128;  // chunks up to which count runs inside the scatter blocks
+
+// Count and scatter in one launch, one workgroup per chunk: every block re-reads the
+// masks of all chunks (nchunks * E * 8 bytes, L2-resident after hist) for each expert's
+// count and this chunk's base, scans the counts into offsets and scatters its chunk;
+// block 0 writes expert_count and expert_offset. The same outputs as count + scatter.
+__global__ __launch_bounds__(DP_THREADS) void dispatch_count_scatter_kernel(DispatchArgs a, int nchunks) {
+  __shared__ int s_off[DP_MAX_E + 1];
+  __shared__ int s_base[DP_MAX_E];
+  __shared__ int s_wsum[DP_THREADS / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = blockIdx.x;
+  const int E = a.E;
+  for (int e = tid; e < E; e += DP_THREADS) {
+    int before = 0, total = 0;
+#pragma unroll 8
+    for (int cc = 0; cc < nchunks; ++cc) {
+      const int v = popc64(a.mask[(size_t)cc * E + e]);
+      before += (cc < c) ? v : 0;
+      total += v;
+    }
+    s_base[e] = before;
+    s_off[e] = total;
+    if (c == 0) a.count[e] = total;
+  }
+  __syncthreads();
+  // expert offsets: exclusive scan of the counts, in place
+  int running = 0;
+  for (int e0 = 0; e0 < E; e0 += DP_THREADS) {
+    const int e = e0 + tid;
+    const int v = (e < E) ? s_off[e] : 0;
+    const int incl = wave_incl_scan(v);
+    if (lane == 63) s_wsum[wave] = incl;
+    __syncthreads();
+    int before = running;
+    for (int w = 0; w < wave; ++w) before += s_wsum[w];
+    int tot = 0;
+    for (int w = 0; w < DP_THREADS / 64; ++w) tot += s_wsum[w];
+    __syncthreads();  // every count of this range is read before the offsets replace them
+    if (e < E) s_off[e] = before + incl - v;
+    running += tot;
+  }
+  if (tid == 0) s_off[E] = running;
+  __syncthreads();
+  if (c == 0)
+    for (int e = tid; e <= E; e += DP_THREADS) a.offset[e] = s_off[e];
+  const int t0 = c * DP_TOK;
+  const int np = min(DP_TOK, a.T - t0) * a.k;
+  const size_t p0 = (size_t)t0 * a.k;
+  for (int i = tid; i < np; i += DP_THREADS) {
+    const size_t p = p0 + i;
+    const int e = a.topk_idx[p];
+    int row = -1;
+    if (e >= 0 && e < E) {
+      const int tl = i / a.k;
+      const uint64_t below = (tl == 0) ? 0ull : (a.mask[(size_t)c * E + e] & ((1ull << tl) - 1ull));
+      row = s_off[e] + s_base[e] + popc64(below);
+      a.row_token[row] = t0 + tl;
+    }
+    a.token_row[p] = row;
+  }
+}
+
 constexpr int DF_THREADS = 1024;
 constexpr size_t DF_MAX_LDS = 144 * 1024;  // masks (8 B) and chunk bases (4 B) of every (chunk, expert)
 constexpr int64_t DF_MAX_PAIRS = 8192;      // (token, slot) pairs up to which one workgroup is used
@@ -213,8 +278,12 @@ hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(dispatch_fused_kernel, dim3(1), dim3(DF_THREADS), 0, s, a, nchunks);
   } else {
     hipLaunchKernelGGL(dispatch_hist_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
-    hipLaunchKernelGGL(dispatch_count_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
-    hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
+    if (nchunks <= DC_MAX_CHUNKS) {
+      hipLaunchKernelGGL(dispatch_count_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a, nchunks);
+    } else {
+      hipLaunchKernelGGL(dispatch_count_kernel, dim3(a.E), dim3(DP_THREADS), 0, s, a, nchunks);
+      hipLaunchKernelGGL(dispatch_scatter_kernel, dim3(nchunks), dim3(DP_THREADS), 0, s, a);
+    }
   }
   if (a.x_perm) {
     const int nrows = a.T * a.k;
