@@ -299,6 +299,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
 // 4096-token batch: 32 experts per block 43 us, 16 experts with 4 stages 38 us, with 6
 // stages 35 us, the register kernel 46 us, top-k included).
 constexpr int RL_TT = 64, RL_NE = 16, RL_BK = 64, RL_D = 6;
+constexpr int RL_THREADS = 256;         // 4 waves: one 16-token row block each
 constexpr int RL_NB = RL_NE / 16;            // 16-expert blocks per wave
 constexpr int RL_XB = RL_TT * RL_BK * 2;     // x bytes per stage (8 KiB)
 constexpr int RL_WB = RL_NE * RL_BK * 4;     // router bytes per stage
@@ -319,7 +320,7 @@ __device__ __forceinline__ void wait_steps(int younger) {
     wait_steps<Y - 1>(younger);
 }
 
-__global__ __launch_bounds__(RT_THREADS) void route_logits_lds_kernel(RouteArgs a, int ntiles, int ngroups) {
+__global__ __launch_bounds__(RL_THREADS) void route_logits_lds_kernel(RouteArgs a, int ntiles, int ngroups) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[RL_D * RL_STAGE];
   __shared__ int s_tau[RL_TT];
   __shared__ int s_first;
@@ -351,7 +352,8 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_lds_kernel(RouteArgs 
   const int H = a.H;
   const int first = s_first;
   auto part = [&](int r) { return a.soft ? s_tau[r] >= 0 : s_tau[r] == pass; };
-  // Copy sources, byte offsets from the step's base. x: copy jj of wave w fills LDS rows
+  // Copy sources, byte offsets from the step's base (x: the tile's first row, so every
+  // offset is below 64 rows of H bf16 whatever T). x: copy jj of wave w fills LDS rows
   // (2w + jj) * 8 + l / 8, lane l's physical chunk l % 8 holding logical chunk
   // (l % 8) ^ ((row >> 1) & 7); a row whose token has the other policy (or lies past T)
   // copies the tile's first token of this policy, so a token's x is only ever read for
@@ -363,7 +365,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_lds_kernel(RouteArgs 
   for (int jj = 0; jj < 2; ++jj) {
     const int r = (2 * wave + jj) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((r >> 1) & 7);
-    const int tok = t0 + (part(r) ? r : first);
+    const int tok = part(r) ? r : first;  // row within the tile
     offx[jj] = ((uint32_t)tok * (uint32_t)H + c * 8) * 2;
   }
   uint32_t offw[RL_WDMA];
@@ -374,7 +376,7 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_lds_kernel(RouteArgs 
     const int n = n0 + r;
     offw[jj] = ((uint32_t)(n < N ? n : n0) * (uint32_t)H + c * 4) * 4;
   }
-  const uint16_t* x = (const uint16_t*)a.x;
+  const uint16_t* x = (const uint16_t*)a.x + (size_t)t0 * H;
   const float* wr = pass ? a.wr_priv : a.wr_pub;
   const int nsteps = H / RL_BK;
   const int rot = (tile * 5 + grp * 3) % nsteps;  // concurrent blocks read different columns
@@ -498,16 +500,12 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   if (a.act_bf16) {
-    const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
-    // the LDS kernel addresses x with 32-bit byte offsets from the step's base
-    if (a.T > 2048 && (uint64_t)a.T * a.H * 2 < (1ull << 32)) {
+    if (a.T > 2048) {
       const int nt = (a.T + RL_TT - 1) / RL_TT;
       const int lgroups = (a.n_pub + RL_NE - 1) / RL_NE + (a.n_priv + RL_NE - 1) / RL_NE;
-      hipLaunchKernelGGL(route_logits_lds_kernel, dim3((nt * lgroups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, lgroups);
-    } else if (a.T > 2048) {
-      const int nt = (a.T + 31) / 32;
-      hipLaunchKernelGGL(route_logits_bf16_kernel<32>, dim3((nt * groups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, groups);
+      hipLaunchKernelGGL(route_logits_lds_kernel, dim3((nt * lgroups + 7) / 8 * 8), dim3(RL_THREADS), 0, s, a, nt, lgroups);
     } else {
+      const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
       const int nt = (a.T + 15) / 16;
       hipLaunchKernelGGL(route_logits_bf16_kernel<16>, dim3((nt * groups + 7) / 8 * 8), dim3(RT_THREADS), 0, s, a, nt, groups);
     }
