@@ -299,13 +299,13 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
 // 4096-token batch: 32 experts per block 43 us, 16 experts with 4 stages 38 us, with 6
 // stages 35 us, the register kernel 46 us, top-k included).
 constexpr int RL_TT = 64, RL_NE = 16, RL_BK = 64, RL_D = 6;
-constexpr int RL_THREADS = 256;         // 4 waves: one 16-token row block each
-constexpr int RL_NB = RL_NE / 16;            // 16-expert blocks per wave
-constexpr int RL_XB = RL_TT * RL_BK * 2;     // x bytes per stage (8 KiB)
-constexpr int RL_WB = RL_NE * RL_BK * 4;     // router bytes per stage
+constexpr int RL_THREADS = 256;                   // 4 waves: one 16-token row block each
+constexpr int RL_NB = RL_NE / 16;                      // 16-expert blocks per wave
+constexpr int RL_XB = RL_TT * RL_BK * 2;               // x bytes per stage (8 KiB)
+constexpr int RL_WB = RL_NE * RL_BK * 4;               // router bytes per stage
 constexpr int RL_STAGE = RL_XB + RL_WB;
-constexpr int RL_WDMA = RL_WB / 1024 / 4;    // router copies per wave per stage (4 rows each)
-constexpr int RL_NDMA = 2 + RL_WDMA;         // copies per wave per stage: 2 of x, the router's
+constexpr int RL_WDMA = RL_WB / 1024 / (RL_THREADS / 64);  // router copies (1 KiB, 4 rows) per wave per stage
+constexpr int RL_NDMA = 2 + RL_WDMA;                   // copies per wave per stage: 2 of x, the router's
 static_assert(RL_NE % 16 == 0 && RL_WDMA >= 1, "router tile");
 
 // Wait for the copies of the oldest step in flight: `younger` steps were issued after it
