@@ -99,10 +99,12 @@ def test_small_bf16_layer(shape, gather):
 
 
 # Batches above 2048 tokens take the router whose operands are staged in LDS (64-token
-# tiles): a ragged last tile, tiles that mix allow and deny tokens (request boundaries off
+# tiles; 2048 tokens is the register kernel's largest batch): a ragged last tile, tiles that mix allow and deny tokens (request boundaries off
 # the 64-token grid), pools that are not multiples of 16, and H = 384 (6 K steps, so the
 # per-block K rotation wraps at an odd count).
 LARGE_ROUTE = [
+    dict(tokens=2048, requests=7, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),  # last register-path size
+    dict(tokens=2049, requests=7, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),  # one-token last tile
     dict(tokens=2113, requests=9, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),
     dict(tokens=4100, requests=5, hidden=384, inter=128, n_pub=128, n_priv=32, top_k=8),
 ]
