@@ -164,8 +164,11 @@ pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const
  *
  * Rows of expert e are the tokens that selected e, in ascending token order; experts
  * are laid out in ascending id order. Deterministic (no order-dependent atomics).
+ * Ids outside [0, E) get no row (token_row = -1) and are not counted. A token that
+ * lists the same expert in several slots gets one row for it, in the first such slot;
+ * the later slots get token_row = -1 (pmpe_route never repeats an id).
  *
- *   topk_idx       [T, k] int32 from pmpe_route
+ *   topk_idx       [T, k] int32 from pmpe_route (or any caller-built index)
  *   x              [T, H] act_dtype (read only if x_perm != NULL)
  *   expert_count   [E] int32 out, E = n_pub + n_priv
  *   expert_offset  [E + 1] int32 out: exclusive prefix sum of expert_count

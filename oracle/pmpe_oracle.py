@@ -309,6 +309,8 @@ class LayerResult:
     tokens: np.ndarray            # evaluated token ids
     hook: ExecutionHook
     expert_count: np.ndarray      # [E]
+    # (token, expert) -> that expert's output row for the token, before the gate
+    y: Dict[tuple, np.ndarray] = field(default_factory=dict)
 
 
 def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_priv, w2_priv,
@@ -329,7 +331,7 @@ def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_pri
     hook = ExecutionHook(T, n_priv)
     y: Dict[tuple, np.ndarray] = {}
     for e in range(E):
-        rows = np.asarray([t for t in toks if e in rt.idx[t]], np.int64)
+        rows = toks[(rt.idx[toks] == e).any(axis=1)]   # the evaluated tokens that selected e
         if len(rows) == 0:
             continue
         X = x[rows]
@@ -349,7 +351,7 @@ def layer_forward(x: np.ndarray, wr_pub, wr_priv, bias, w13_pub, w2_pub, w13_pri
         if ysh is not None:
             acc += ysh[i]
         out[i] = acc
-    return LayerResult(rt, dp, out, toks, hook, dp.count)
+    return LayerResult(rt, dp, out, toks, hook, dp.count, y)
 
 
 # ----------------------------------------------------------------------------

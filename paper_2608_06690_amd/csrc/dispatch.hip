@@ -19,7 +19,9 @@
 // bases fit in LDS run hist, count and scatter back to back in one workgroup
 // (dispatch_fused_kernel): one launch instead of three, and the same outputs.
 // No order-dependent atomics: the permutation is deterministic. Expert ids outside
-// [0, E) are not counted and get token_row = -1.
+// [0, E) are not counted and get token_row = -1. A token lists an expert at most once:
+// if its row repeats an id, the first slot holding it gets the row and every later
+// slot gets token_row = -1 (the router never repeats an id; a caller-built index may).
 #include "pmpe_internal.h"
 
 namespace pmpe {
@@ -30,6 +32,13 @@ constexpr int DP_THREADS = 256;
 constexpr int DP_MAX_E = 2 * PMPE_MAX_POOL;
 
 __device__ __forceinline__ int popc64(uint64_t v) { return __popcll(v); }
+
+// Does slot j of a token's id row (ids[0..k)) repeat an id of an earlier slot?
+__device__ __forceinline__ bool repeats_earlier(const int32_t* ids, int j, int e) {
+  for (int i = 0; i < j; ++i)
+    if (ids[i] == e) return true;
+  return false;
+}
 
 __global__ __launch_bounds__(DP_THREADS) void dispatch_hist_kernel(DispatchArgs a) {
   __shared__ unsigned long long s_mask[DP_MAX_E];
@@ -108,8 +117,8 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_scatter_kernel(DispatchAr
     const size_t p = p0 + i;
     const int e = a.topk_idx[p];
     int row = -1;
-    if (e >= 0 && e < E) {
-      const int tl = i / a.k;
+    const int tl = i / a.k, j = i - tl * a.k;
+    if (e >= 0 && e < E && !repeats_earlier(a.topk_idx + (p - j), j, e)) {
       const uint64_t below = (tl == 0) ? 0ull : (a.mask[(size_t)c * E + e] & ((1ull << tl) - 1ull));
       row = s_off[e] + a.chunk_base[(size_t)c * E + e] + popc64(below);
       a.row_token[row] = t0 + tl;
@@ -171,8 +180,8 @@ __global__ __launch_bounds__(DP_THREADS) void dispatch_count_scatter_kernel(Disp
     const size_t p = p0 + i;
     const int e = a.topk_idx[p];
     int row = -1;
-    if (e >= 0 && e < E) {
-      const int tl = i / a.k;
+    const int tl = i / a.k, j = i - tl * a.k;
+    if (e >= 0 && e < E && !repeats_earlier(a.topk_idx + (p - j), j, e)) {
       const uint64_t below = (tl == 0) ? 0ull : (a.mask[(size_t)c * E + e] & ((1ull << tl) - 1ull));
       row = s_off[e] + s_base[e] + popc64(below);
       a.row_token[row] = t0 + tl;
@@ -240,8 +249,9 @@ __global__ __launch_bounds__(DF_THREADS) void dispatch_fused_kernel(DispatchArgs
   for (int p = tid; p < np; p += DF_THREADS) {
     const int e = a.topk_idx[p];
     int row = -1;
-    if (e >= 0 && e < E) {
-      const int t = p / k, c = t / DP_TOK, tl = t % DP_TOK;
+    const int t = p / k, j = p - t * k;
+    if (e >= 0 && e < E && !repeats_earlier(a.topk_idx + (p - j), j, e)) {
+      const int c = t / DP_TOK, tl = t % DP_TOK;
       const uint64_t below = (tl == 0) ? 0ull : (s_mask[c * E + e] & ((1ull << tl) - 1ull));
       row = s_off[e] + s_base[c * E + e] + popc64(below);
       a.row_token[row] = t;

@@ -77,24 +77,13 @@ struct Cfg {
   static_assert(A_DMA * RPD * WAVES == BM && B_DMA * RPD_B * WAVES == BN, "DMA split");
   static_assert(!W8 || BK == 64, "fp8 weight rows are 64 bytes");
 };
-#ifndef PMPE_CFG_LARGE
-#define PMPE_CFG_LARGE 256, 256, 4, 2, 2, 64
-#endif
-#ifndef PMPE_CFG_SMALL
-#define PMPE_CFG_SMALL 64, 128, 1, 4, 3, 64, 2, true, true
-#endif
-using CfgLarge = Cfg<PMPE_CFG_LARGE>;  // prefill: 8 waves of 64 x 128, 2 x 64 KiB stages
-using CfgSmall = Cfg<PMPE_CFG_SMALL>;  // decode-shaped: 4 waves, 3 x 24 KiB stages, streamed weights
+using CfgLarge = Cfg<256, 256, 4, 2, 2, 64>;  // prefill: 8 waves of 64 x 128, 2 x 64 KiB stages
+// decode-shaped: 4 waves, 3 x 24 KiB stages, streamed weights
+using CfgSmall = Cfg<64, 128, 1, 4, 3, 64, 2, true, true>;
 // fp8 weights: the smaller weight tiles leave room for a third stage (3 x 48 KiB) in the
 // prefill configuration and for three resident blocks per CU in the decode one
-#ifndef PMPE_CFG_LARGE8
-#define PMPE_CFG_LARGE8 256, 256, 4, 2, 3, 64, 1, true, false, true
-#endif
-#ifndef PMPE_CFG_SMALL8
-#define PMPE_CFG_SMALL8 64, 128, 1, 4, 3, 64, 2, true, true, true
-#endif
-using CfgLarge8 = Cfg<PMPE_CFG_LARGE8>;
-using CfgSmall8 = Cfg<PMPE_CFG_SMALL8>;
+using CfgLarge8 = Cfg<256, 256, 4, 2, 3, 64, 1, true, false, true>;
+using CfgSmall8 = Cfg<64, 128, 1, 4, 3, 64, 2, true, true, true>;
 
 constexpr int MAXG = 2 * PMPE_MAX_POOL + 1;  // routed experts + the shared group
 
@@ -142,7 +131,12 @@ struct TileInfo {
 template <class C, bool GATED, bool SAVE = false, bool AUDIT = true>
 __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
-  __shared__ __attribute__((aligned(16))) int s_rt[3][C::BM];
+  // Gather-index slices (row_token) of the tiles in flight. The producer runs up to
+  // STAGES-1 K steps ahead of the consumer and fetches a tile's slice one tile before its
+  // first step, so with one K step per tile (K = BK) the slices of tiles ci .. ci+STAGES
+  // are live while tile ci is consumed: STAGES+1 slots.
+  constexpr int NRT = C::STAGES + 1;
+  __shared__ __attribute__((aligned(16))) int s_rt[NRT][C::BM];
   __shared__ int s_cum[MAXG + 1];
   __shared__ int s_cnt[MAXG];
   __shared__ int s_off[MAXG];
@@ -353,8 +347,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
       pk = 0;
       if (pi >= ntl) return;
       pt = tile_of(pi);
-      pnk = setup_ctx(pt, pi % 3);
-      if (pi + 1 < ntl) issue_rt(tile_of(pi + 1), (pi + 1) % 3);
+      pnk = setup_ctx(pt, pi % NRT);
+      if (pi + 1 < ntl) issue_rt(tile_of(pi + 1), (pi + 1) % NRT);
     }
     issue(slot, pk * BK);
     ++pk;
@@ -558,7 +552,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     }
     // Execution audit: the first N tile of every executed private M tile counts its rows.
     if (!GATED && AUDIT && c_priv && c_valid && ct.n0 == 0) {
-      for (int r = tid; r < ct.rows; r += C::THREADS) atomicAdd(&a.audit_rows[s_rt[ci % 3][r]], 1u);
+      for (int r = tid; r < ct.rows; r += C::THREADS) atomicAdd(&a.audit_rows[s_rt[ci % NRT][r]], 1u);
       if (ct.m0 == 0 && tid == 0 && a.audit_calls) atomicAdd(&a.audit_calls[ct.g - a.n_pub], 1u);
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)

@@ -618,6 +618,25 @@ def test_backward_equals_autograd_of_textbook_forward(mode, soft, shared):
     assert np.all(np.abs(g.dw13_priv[used]).sum(axis=(1, 2)) > 0)
 
 
+def test_backward_square_expert_equals_autograd():
+    """H == I, so a transposed expert weight still has the right shape: only the values
+    can catch it. Autograd of the textbook forward, both gate modes."""
+    import torch
+    for mode in ("renorm", "pool_softmax"):
+        c, taus, words, mode, soft, k = _bwd_case(15, mode, H=8, I=8)
+        g = _oracle_grads(c, words, mode, soft, k)
+        tt = {n: (None if v is None else torch.tensor(v, dtype=torch.float64, requires_grad=True))
+              for n, v in c.items()}
+        out, _ = _textbook_layer_torch(tt["x"], tt["wr_pub"], tt["wr_priv"], tt["bias"], tt["w13_pub"],
+                                       tt["w2_pub"], tt["w13_priv"], tt["w2_priv"], taus, k, mode)
+        (out * tt["dout"]).sum().backward()
+        rel = lambda a, b: np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)  # noqa: E731
+        assert rel(g.dx, tt["x"].grad.numpy()) < 1e-6
+        assert rel(g.dw13_priv, tt["w13_priv"].grad.numpy()) < 1e-6
+        assert rel(g.dw2_priv, tt["w2_priv"].grad.numpy()) < 1e-6
+        assert rel(g.dwr_priv, tt["wr_priv"].grad.numpy()) < 1e-6
+
+
 def test_backward_central_differences():
     """A few entries of each gradient against (L(p + e) - L(p - e)) / 2e of the fp64
     textbook forward, L = sum(dout * out)."""
@@ -751,6 +770,35 @@ def test_lora_physical_rows_by_gate():
                 for t in blk:
                     brute[t] += 1
     assert np.array_equal(tile, brute)
+
+
+def test_lora_tile_gate_known_by_construction():
+    """Tile gate on a routing whose dispatch order is known without running dispatch:
+    k = 1, tokens 0..99 select expert 0 and tokens 100..229 expert 1, so expert 0's rows
+    are tokens 0..99 (tiles 0..63 and 64..99) and expert 1's are 100..229 (tiles 100..163,
+    164..227, 228..229). Allowed tokens: 10 (first tile of expert 0), 200 (second tile of
+    expert 1), 229 (last tile of expert 1). Exactly the rows of those three tiles run the
+    adapter, one row each; with k = 2 and the same tokens on both experts (expert ids
+    0 and 1 for every token), every tile holding token 10 runs, on both experts."""
+    T = 230
+    idx = np.zeros((T, 1), np.int64)
+    idx[100:, 0] = 1
+    taus = np.zeros(T, np.int64)
+    taus[[10, 200, 229]] = 1
+    tile = O.lora_physical_rows(idx, taus, 2, O.LORA_GATE_TILE)
+    expect = np.zeros(T, np.int64)
+    expect[0:64] = 1          # expert 0, tile of rows 0..63 (token 10)
+    expect[164:228] = 1       # expert 1, tile of tokens 164..227 (token 200)
+    expect[228:230] = 1       # expert 1, tile of tokens 228..229 (token 229)
+    assert np.array_equal(tile, expect)
+    idx2 = np.tile(np.array([[0, 1]]), (T, 1))
+    taus2 = np.zeros(T, np.int64)
+    taus2[10] = 1
+    tile2 = O.lora_physical_rows(idx2, taus2, 2, O.LORA_GATE_TILE)
+    expect2 = np.zeros(T, np.int64)
+    expect2[0:64] = 2         # tokens 0..63 form the first tile of both experts
+    assert np.array_equal(tile2, expect2)
+    assert np.array_equal(O.lora_physical_rows(idx2, taus2, 2, O.LORA_GATE_ROW), 2 * taus2)
 
 
 def test_adamw_step_equals_torch_adamw():

@@ -194,7 +194,8 @@ def normal(key: int, shape: Sequence[int], std: float, dtype: torch.dtype = torc
         z = (z ^ _lsr(z, 30)) * _signed(_MIX1)
         z = (z ^ _lsr(z, 27)) * _signed(_MIX2)
         z = z ^ _lsr(z, 31)
-        u = torch.stack([(z >> (16 * i)) & 0xFFFF for i in range(4)], dim=1).reshape(-1)
+        # the four 16-bit fields of each word, lowest first (little-endian lanes)
+        u = z.view(torch.int16).to(torch.int32) & 0xFFFF
         e0 = 4 * w0
         e1 = min(n, 4 * (w0 + nw))
         v = table[u[: e1 - e0]] * scale
