@@ -58,7 +58,8 @@ typedef enum {
   PMPE_ERR_ALIGN = -5,           /* a pointer is not 16-byte aligned */
   PMPE_ERR_WORKSPACE = -6,       /* workspace missing or smaller than pmpe_workspace_bytes */
   PMPE_ERR_LAUNCH = -7,          /* the HIP runtime refused a launch */
-  PMPE_ERR_TAG_MISMATCH = -8     /* a cache tag does not match the request (reuse refused) */
+  PMPE_ERR_TAG_MISMATCH = -8,    /* a cache tag does not match the request (reuse refused) */
+  PMPE_ERR_SCRATCH = -9          /* needs more scratch than the allocation-free entry holds */
 } pmpe_status;
 
 typedef enum { PMPE_F32 = 0, PMPE_BF16 = 1, PMPE_FP8_E4M3 = 2 } pmpe_dtype;
@@ -182,6 +183,27 @@ pmpe_status pmpe_dispatch(const pmpe_layer_desc* d, int32_t T, const int32_t* to
                           const void* x, int32_t* expert_count, int32_t* expert_offset,
                           int32_t* row_token, int32_t* token_row, void* x_perm, void* ws,
                           size_t ws_bytes, pmpe_stream_t stream);
+
+/*
+ * pmpe_dispatch_noalloc - pmpe_dispatch without a workspace argument.
+ * For callers that cannot allocate device memory: code under HIP graph capture, serving
+ * loops and harnesses that forbid hipMalloc.
+ *
+ * Same outputs, arguments (minus ws / ws_bytes), validation and errors as pmpe_dispatch.
+ * Its per-chunk expert masks and chunk bases live in a file-scope device array of
+ * PMPE_NOALLOC_SCRATCH_BYTES on each GPU the library runs on, held until the process
+ * ends; a batch needing more (about T / 64 * (n_pub + n_priv) * 12 bytes) returns
+ * PMPE_ERR_SCRATCH before anything is launched. Calls no hipMalloc, hipFree or other
+ * allocating routine; the first call on a device (the current device, which must be the
+ * stream's) looks up that device's copy of the array once. Every call on one GPU uses
+ * that GPU's single array: calls that overlap on one GPU (two streams, two threads)
+ * race. Nothing in the array has to start at zero: every call writes what it reads.
+ */
+#define PMPE_NOALLOC_SCRATCH_BYTES ((size_t)2 << 20)
+pmpe_status pmpe_dispatch_noalloc(const pmpe_layer_desc* d, int32_t T, const int32_t* topk_idx,
+                                  const void* x, int32_t* expert_count, int32_t* expert_offset,
+                                  int32_t* row_token, int32_t* token_row, void* x_perm,
+                                  pmpe_stream_t stream);
 
 /*
  * pmpe_expert_ffn - run every expert with at least one row, and the shared group.

@@ -14,6 +14,7 @@ from ._native import (PMPE_BF16, PMPE_F32, PMPE_GATE_POOL_SOFTMAX, PMPE_GATE_REN
                       PMPE_LORA_TILE_ROWS, pmpe_expert_ffn_lora, pmpe_expert_ffn_lora_workspace_bytes,
                       pmpe_adamw, pmpe_transpose_experts, PMPE_FP8_E4M3, pmpe_expert_ffn_fp8,
                       pmpe_audit, pmpe_check_desc, pmpe_combine, pmpe_dispatch, pmpe_expert_ffn,
+                      pmpe_dispatch_noalloc, PMPE_ERR_SCRATCH, PMPE_NOALLOC_SCRATCH_BYTES,
                       pmpe_route, pmpe_version, pmpe_workspace_bytes)
 from .layer import (AuditBuffers, GradBuffers, LayerBuffers, PolicyMaskedMoE,  # noqa: F401
                     PrivateAdamW)

@@ -41,9 +41,11 @@ PMPE_DEV_PRIV_WEIGHTS_MISSING = 0x2
 STATUS_NAMES = {
     0: "PMPE_OK", -1: "PMPE_ERR_NULL", -2: "PMPE_ERR_SHAPE", -3: "PMPE_ERR_K_EXCEEDS_POOL",
     -4: "PMPE_ERR_DTYPE", -5: "PMPE_ERR_ALIGN", -6: "PMPE_ERR_WORKSPACE", -7: "PMPE_ERR_LAUNCH",
-    -8: "PMPE_ERR_TAG_MISMATCH",
+    -8: "PMPE_ERR_TAG_MISMATCH", -9: "PMPE_ERR_SCRATCH",
 }
 PMPE_ERR_TAG_MISMATCH = -8
+PMPE_ERR_SCRATCH = -9
+PMPE_NOALLOC_SCRATCH_BYTES = 2 << 20
 PMPE_LORA_GATE_ROW = 0
 PMPE_LORA_GATE_TILE = 1
 PMPE_LORA_GATE_POSTHOC = 2
@@ -100,6 +102,8 @@ _lib.pmpe_route.restype = _I32
 _lib.pmpe_route.argtypes = [_DESC, _I32] + [_P] * 10 + [_P, _SZ, _P]
 _lib.pmpe_dispatch.restype = _I32
 _lib.pmpe_dispatch.argtypes = [_DESC, _I32] + [_P] * 7 + [_P, _SZ, _P]
+_lib.pmpe_dispatch_noalloc.restype = _I32
+_lib.pmpe_dispatch_noalloc.argtypes = [_DESC, _I32] + [_P] * 7 + [_P]
 _lib.pmpe_expert_ffn.restype = _I32
 _lib.pmpe_expert_ffn.argtypes = [_DESC, _I32] + [_P] * 16 + [_P, _SZ, _P]
 _lib.pmpe_combine.restype = _I32
@@ -202,6 +206,15 @@ def pmpe_dispatch(desc, T, topk_idx, x, expert_count, expert_offset, row_token, 
                               _ptr(expert_offset), _ptr(row_token), _ptr(token_row), _ptr(x_perm),
                               _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                               _stream(stream)), "pmpe_dispatch")
+
+
+def pmpe_dispatch_noalloc(desc, T, topk_idx, x, expert_count, expert_offset, row_token, token_row,
+                          x_perm, stream=None) -> None:
+    """pmpe_dispatch with the library's own per-device scratch array (no workspace)."""
+    _check(_lib.pmpe_dispatch_noalloc(ctypes.byref(desc), T, _ptr(topk_idx), _ptr(x),
+                                      _ptr(expert_count), _ptr(expert_offset), _ptr(row_token),
+                                      _ptr(token_row), _ptr(x_perm), _stream(stream)),
+           "pmpe_dispatch_noalloc")
 
 
 def pmpe_expert_ffn(desc, T, x_perm, x, expert_count, expert_offset, row_token, w13_pub, w2_pub,

@@ -174,6 +174,10 @@ pmpe_status expert_ffn_impl(const pmpe_layer_desc* d, int32_t T, const void* x_p
 
 }  // namespace
 
+namespace pmpe {
+size_t dispatch_workspace_bytes(const pmpe_layer_desc* d, int32_t T) { return dispatch_ws(d, T); }
+}  // namespace pmpe
+
 extern "C" {
 
 int32_t pmpe_version(void) { return 10000; }
@@ -189,6 +193,8 @@ const char* pmpe_status_string(int32_t status) {
     case PMPE_ERR_WORKSPACE: return "workspace missing or too small";
     case PMPE_ERR_LAUNCH: return "the HIP runtime refused a kernel launch";
     case PMPE_ERR_TAG_MISMATCH: return "cache tag does not match the request; reuse refused";
+    case PMPE_ERR_SCRATCH:
+      return "the batch needs more scratch than the allocation-free entry point holds";
     default: return "unknown status";
   }
 }

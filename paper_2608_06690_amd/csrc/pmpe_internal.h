@@ -112,6 +112,8 @@ struct DispatchArgs {
 };
 int dispatch_chunks(int T);
 hipError_t launch_dispatch(const DispatchArgs& a, hipStream_t s);
+// workspace pmpe_dispatch needs for a valid descriptor (its masks and chunk bases)
+size_t dispatch_workspace_bytes(const pmpe_layer_desc* d, int32_t T);
 
 struct FfnArgs {
   int T, H, I, n_pub, n_priv, k, act_bf16;

@@ -261,3 +261,29 @@ def test_fp8_entry_validation():
     assert lib.pmpe_expert_ffn_fp8(ctypes.byref(d8), 16, *p2, 0x20000, 1 << 20, None) == -1
     # workspace too small
     assert lib.pmpe_expert_ffn_fp8(ctypes.byref(d8), 16, *ptrs, 0x20000, 16, None) == -6
+
+
+def test_noalloc_dispatch_validation_before_the_device():
+    """pmpe_dispatch_noalloc rejects a batch whose masks and chunk bases exceed its scratch
+    array (PMPE_ERR_SCRATCH), a NULL output and a bad descriptor, all before it touches a
+    device (these calls run with no GPU)."""
+    lib = N.lib()
+    d = desc(n_pub=256, n_priv=256)               # 512 experts: 12 bytes per (chunk, expert)
+    chunks = N.PMPE_NOALLOC_SCRATCH_BYTES // (512 * 12)
+    too_big = 64 * (chunks + 1)
+    st = lib.pmpe_dispatch_noalloc(ctypes.byref(d), too_big, 0x1000, None, 0x3000, 0x4000, 0x5000,
+                                   0x6000, None, None)
+    assert st == N.PMPE_ERR_SCRATCH == -9
+    assert "scratch" in lib.pmpe_status_string(-9).decode()
+    st = lib.pmpe_dispatch_noalloc(ctypes.byref(d), 64, None, None, 0x3000, 0x4000, 0x5000, 0x6000,
+                                   None, None)
+    assert st == -1
+    st = lib.pmpe_dispatch_noalloc(ctypes.byref(desc(top_k=0)), 64, 0x1000, None, 0x3000, 0x4000,
+                                   0x5000, 0x6000, None, None)
+    assert st == -2
+    # the Qwen-shaped batches (160 experts) fit up to 69,888 tokens
+    q = desc()
+    assert (4096 + 63) // 64 * 160 * 12 <= N.PMPE_NOALLOC_SCRATCH_BYTES
+    st = lib.pmpe_dispatch_noalloc(ctypes.byref(q), 64 * (N.PMPE_NOALLOC_SCRATCH_BYTES // (160 * 12) + 2),
+                                   0x1000, None, 0x3000, 0x4000, 0x5000, 0x6000, None, None)
+    assert st == -9
