@@ -15,6 +15,7 @@ import torch
 import workloads as W
 from oracle import pmpe_oracle as O
 from tests import pmpe_cases as C
+import paper_2608_06690_amd as P
 
 pytestmark = pytest.mark.gpu
 
@@ -201,3 +202,67 @@ def test_decode_layer_full_oracle():
     assert req.kinds.count("malformed") == 26 and req.kinds.count("allow") == 64
     d, ref = full_check(cfg, layer, x, words, req)
     assert int(d.allow.sum()) == 64
+
+
+# ----------------------------------------------------------------------------
+# Prefill batches on the 256 x 256 persistent expert kernel (T*k at least 128 rows per
+# expert on average): several tiles per persistent block, ragged M tiles (private
+# experts of ~2,460 rows, public ones of ~820), rows past a tile's valid count, both
+# gather paths, the shared group, and the fail-closed paths (NULL or NaN private
+# weights) at this size
+# ----------------------------------------------------------------------------
+
+PREFILL_MULTI = dict(tokens=4100, requests=5, hidden=1024, inter=512, n_pub=16, n_priv=8, top_k=8)
+
+
+@pytest.mark.parametrize("gather", [False, True], ids=["fused_gather", "dispatch_gather"])
+def test_prefill_multi_tile(gather):
+    cfg = W.scaled_config(W.get_config("qwen"), **PREFILL_MULTI)
+    layer, _ = C.device_layer(cfg, gather_in_dispatch=gather)
+    x = W.make_x(cfg, "cuda")
+    req = W.alternating_requests(cfg.requests, cfg.tokens // cfg.requests)
+    words = O.compile_words(req.metas, req.lengths)
+    d, ref = full_check(cfg, layer, x, words, req)
+    cnt = ref.disp.count
+    assert cnt[cfg.n_pub:].min() > 2 * 256 and cnt[:cfg.n_pub].min() > 256   # ragged multi-tile experts
+
+
+def test_prefill_shared_group_pool_softmax():
+    cfg = W.scaled_config(W.get_config("deepseek"), tokens=2048, requests=4, hidden=512, inter=256,
+                          n_pub=32, n_priv=8, top_k=6, shared_inter=128)
+    assert cfg.n_shared * cfg.shared_inter == 256
+    layer, _ = C.device_layer(cfg)
+    x = W.make_x(cfg, "cuda")
+    req, words = words_for(cfg)
+    full_check(cfg, layer, x, words, req)
+
+
+def test_prefill_fail_closed_private_weights():
+    cfg = W.scaled_config(W.get_config("qwen"), **PREFILL_MULTI)
+    x = W.make_x(cfg, "cuda")
+    req = W.alternating_requests(cfg.requests, cfg.tokens // cfg.requests)
+    words = O.compile_words(req.metas, req.lengths)
+    offs = torch.tensor(req.offsets, device="cuda")
+    ref_layer, Lw = C.device_layer(cfg)
+    ref = C.run_device(ref_layer, x, C.words_tensor(words), offs)
+    # allow rows with the private weights missing: not executed, not audited, zeroed
+    nul = P.PolicyMaskedMoE(C.make_desc(cfg), Lw.wr_pub, Lw.wr_priv, None, Lw.w13_pub, Lw.w2_pub,
+                            None, None)
+    d = C.run_device(nul, x, C.words_tensor(words), offs)
+    taus = np.array([O.decode_word(w) for w in words])
+    assert d.dev_status & 0x2 and d.total == 0 and d.audit_rows.sum() == 0
+    assert torch.all(d.out[torch.from_numpy(taus == 1)] == 0)
+    deny = torch.from_numpy(taus == 0)
+    assert torch.equal(d.out[deny], ref.out[deny])
+    # all deny: NULL and NaN private tensors give the full layer's output bit for bit
+    dreq = W.Requests([820] * 5, [W.DENY_META] * 5, ["deny"] * 5)
+    dwords = C.words_tensor(O.compile_words(dreq.metas, dreq.lengths))
+    base = C.run_device(ref_layer, x, dwords, offs)
+    nulld = C.run_device(C.device_layer(cfg, drop_private=True)[0], x, dwords, offs)
+    nan = P.PolicyMaskedMoE(C.make_desc(cfg), Lw.wr_pub, torch.full_like(Lw.wr_priv, float("nan")), None,
+                            Lw.w13_pub, Lw.w2_pub, torch.full_like(Lw.w13_priv, float("nan")),
+                            torch.full_like(Lw.w2_priv, float("nan")))
+    dnan = C.run_device(nan, x, dwords, offs)
+    for dd in (nulld, dnan):
+        assert torch.equal(dd.out, base.out) and dd.total == 0 and dd.dev_status == 0
+    log(f"prefill fail-closed: allow rows zeroed {int((taus == 1).sum())}, deny rows equal")
