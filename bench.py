@@ -43,7 +43,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
 # counters were taken on: any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "d3683543e3e1083596bb166b769dea0c13abb6c60f867c53779ad6744da7f38b": 2_008_443_886,
+    "7b63674b06361163fc6430fb1615ce68724240b739db14f7da767a0b81ddb6fe": 1_985_500_173,
 }
 
 
@@ -85,6 +85,8 @@ def parse():
     p.add_argument("--no-private-weights", action="store_true",
                    help="with --all-deny: pass NULL for every private tensor (router rows and "
                         "expert weights); the counters must read the same bytes as with them present")
+    p.add_argument("--deepseek-only", action="store_true",
+                   help="time only the DeepSeek-V2-Lite-shaped layer (for a separate kernel profile)")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="run only a plain 1 GiB device-to-device copy (counter calibration)")
     return p.parse_args()
@@ -582,6 +584,9 @@ def main():
         return
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
+        return
+    if args.deepseek_only:
+        print(json.dumps(deepseek_bench(args, dev)), flush=True)
         return
     if args.fp8_only:
         print(json.dumps(fp8_bench(args, dev)), flush=True)
