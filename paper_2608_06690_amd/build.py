@@ -61,6 +61,73 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host-side checking build: the sources that hold the C ABI's argument validation
+# (every check runs on the host before anything reaches a device) are compiled with
+# AddressSanitizer and UndefinedBehaviorSanitizer on their host pass only; the device
+# code and the other objects are the ordinary ones. The result is a second library,
+# never loaded by the package, that a CPU test drives through the error paths with the
+# sanitizer runtime preloaded.
+SAN_DIR = os.path.join(BUILD_DIR, "san")
+SAN_LIB = os.path.join(SAN_DIR, "libpmpe_san.so")
+SAN_SRCS = ("pmpe_api.hip", "noalloc.hip")
+SAN_FLAGS = ["-O1", "-g",
+             "-Xarch_host", "-fsanitize=address,undefined",
+             "-Xarch_host", "-fno-sanitize-recover=all",
+             "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def sanitizer_runtime() -> str:
+    """Path of the clang AddressSanitizer runtime that a process loading SAN_LIB preloads."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "lib", "llvm", "bin", "clang")
+    for cand in (clang, "/opt/rocm/lib/llvm/bin/clang", shutil.which("clang") or ""):
+        if cand and os.path.exists(cand):
+            r = subprocess.run([cand, "-print-file-name=libclang_rt.asan-x86_64.so"],
+                               capture_output=True, text=True)
+            path = r.stdout.strip()
+            if r.returncode == 0 and os.path.isabs(path) and os.path.exists(path):
+                return path
+    raise RuntimeError("the clang AddressSanitizer runtime was not found")
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """Link SAN_LIB from the validation sources built with the host sanitizers and the
+    ordinary objects of every other source; rebuilt when a source or header is newer."""
+    os.makedirs(SAN_DIR, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    deps = srcs + glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(INCLUDE, "*.h"))
+    newest = max(os.path.getmtime(f) for f in deps + [__file__])
+    if os.path.exists(SAN_LIB) and os.path.getmtime(SAN_LIB) >= newest:
+        return SAN_LIB
+
+    def one(src):
+        name = os.path.basename(src)
+        if name in SAN_SRCS:
+            obj = os.path.join(SAN_DIR, name + ".o")
+            cmd = [hipcc(), *[f for f in COMMON if f != "-O3"], *SAN_FLAGS, "-c", src, "-o", obj]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+            return obj
+        obj = os.path.join(BUILD_DIR, name + ".o")
+        if os.path.exists(obj) and os.path.getmtime(obj) >= newest:
+            return obj
+        return _compile(src)
+
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(one, srcs))
+    tmp = SAN_LIB + f".tmp{os.getpid()}"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address,undefined",
+           "-shared-libasan", "-o", tmp, *objs]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, SAN_LIB)
+    if verbose:
+        print(f"built {SAN_LIB}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)
