@@ -437,7 +437,9 @@ def backward_bench(args, dev):
     opt_us = e0.elapsed_time(e1) * 1e3 / reps
     n_f32 = layer.wr_priv.numel()
     n_bf16 = layer.w13_priv.numel() + layer.w2_priv.numel()
-    opt_bytes = 28 * n_f32 + 30 * n_bf16
+    # the step also remakes the backward's transposed copies of the private experts
+    # (read and write 2 bytes per bf16 weight), once per step instead of once per backward
+    opt_bytes = 28 * n_f32 + 30 * n_bf16 + 4 * n_bf16
     counts = bufs.expert_count.cpu()
     R = cfg.tokens * cfg.top_k
     Rp = int(counts[cfg.n_pub:].sum())
@@ -455,7 +457,8 @@ def backward_bench(args, dev):
            "tflops_algorithmic": alg / (us * 1e-6) / 1e12,
            "tflops_executed": executed / (us * 1e-6) / 1e12,
            "frac_algorithmic": alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, "reps": reps,
-           "optimizer": {"kind": "AdamW over the private parameters only",
+           "optimizer": {"kind": "AdamW over the private parameters only, then the transposed "
+                                 "copies of the private expert weights that the backward uses",
                          "params": n_f32 + n_bf16, "us_per_step": opt_us, "bytes": opt_bytes,
                          "hbm_gbs": opt_bytes / (opt_us * 1e-6) / 1e9,
                          "hbm_frac": opt_bytes / (opt_us * 1e-6) / 1e9 / PEAK_HBM_GBS}}

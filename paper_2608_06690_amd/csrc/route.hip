@@ -285,10 +285,10 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
 }
 
 // Large batches: token-tile x expert-group logits with both operands staged in LDS.
-// Block (tile, g): 64 tokens against RL_NE experts of one pool; wave w owns the tile's
+// Block (tile, g): TT tokens against RL_NE experts of one pool; wave w owns the tile's
 // 16-token row block w over the whole of H, so no partial sums are exchanged. K steps of
-// 64: a step's x rows (64 x 128 bytes) and fp32 router rows (RL_NE x 256 bytes) are copied
-// whole into a ring of RL_D stages by global->LDS copies, so every request is a full
+// 64: a step's x rows (TT x 128 bytes) and fp32 router rows (RL_NE x 256 bytes) are copied
+// whole into a ring of D stages by global->LDS copies, so every request is a full
 // 128-byte line (loads of 64-byte row pieces straight into the MFMA register layout
 // bound the register kernel at this size). The 16-byte chunks of each LDS row are
 // XOR-swizzled by row so that the fragment reads of 16 rows hit distinct banks. Token
@@ -298,50 +298,60 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
 // copies in flight per CU, so more concurrent blocks beat fewer re-reads (Qwen-shaped
 // 4096-token batch: 32 experts per block 43 us, 16 experts with 4 stages 38 us, with 6
 // stages 35 us, the register kernel 46 us, top-k included).
-constexpr int RL_TT = 64, RL_NE = 16, RL_BK = 64, RL_D = 6;
-constexpr int RL_THREADS = 256;                   // 4 waves: one 16-token row block each
-constexpr int RL_NB = RL_NE / 16;                      // 16-expert blocks per wave
-constexpr int RL_XB = RL_TT * RL_BK * 2;               // x bytes per stage (8 KiB)
-constexpr int RL_WB = RL_NE * RL_BK * 4;               // router bytes per stage
-constexpr int RL_STAGE = RL_XB + RL_WB;
-constexpr int RL_WDMA = RL_WB / 1024 / (RL_THREADS / 64);  // router copies (1 KiB, 4 rows) per wave per stage
-constexpr int RL_NDMA = 2 + RL_WDMA;                   // copies per wave per stage: 2 of x, the router's
-static_assert(RL_NE % 16 == 0 && RL_WDMA >= 1, "router tile");
+constexpr int RL_NE = 16, RL_BK = 64;
+template <int TT_, int D_>
+struct RlCfg {
+  static constexpr int TT = TT_, D = D_;
+  static constexpr int THREADS = 4 * TT;                 // one wave per 16-token row block
+  static constexpr int WAVES = THREADS / 64;
+  static constexpr int NB = RL_NE / 16;                  // 16-expert blocks per wave
+  static constexpr int XB = TT * RL_BK * 2;              // x bytes per stage
+  static constexpr int WB = RL_NE * RL_BK * 4;           // router bytes per stage
+  static constexpr int STAGE = XB + WB;
+  static constexpr int WDMA = WB / 1024 / WAVES;         // router copies (1 KiB, 4 rows) per wave per stage
+  static constexpr int NDMA = 2 + WDMA;                  // copies per wave per stage: 2 of x, the router's
+  static_assert(TT % 16 == 0 && RL_NE % 16 == 0 && WDMA >= 1 && WDMA * WAVES * 1024 == WB, "router tile");
+};
+using RlLarge = RlCfg<64, 6>;
 
 // Wait for the copies of the oldest step in flight: `younger` steps were issued after it
-// (RL_NDMA copies each, loads complete in order), at most Y of which may stay in flight.
-template <int Y>
+// (NDMA copies each, loads complete in order), at most Y of which may stay in flight.
+template <int Y, int NDMA>
 __device__ __forceinline__ void wait_steps(int younger) {
   if constexpr (Y == 0)
     wait_vmcnt<0>();
   else if (younger >= Y)
-    wait_vmcnt<Y * RL_NDMA>();
+    wait_vmcnt<Y * NDMA>();
   else
-    wait_steps<Y - 1>(younger);
+    wait_steps<Y - 1, NDMA>(younger);
 }
 
-__global__ __launch_bounds__(RL_THREADS) void route_logits_lds_kernel(RouteArgs a, int ntiles, int ngroups) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[RL_D * RL_STAGE];
-  __shared__ int s_tau[RL_TT];
+// Block b runs on XCD b % 8. Token tiles are dealt round-robin to the XCDs (tile
+// 8 i + x to XCD x) with the groups of one tile adjacent on its XCD, so the blocks
+// that find tokens of their pool spread over all XCDs even when consecutive tiles share
+// a policy (requests are contiguous token ranges), and a tile's x rows are shared in
+// one L2.
+template <class R>
+__global__ __launch_bounds__(R::THREADS) void route_logits_lds_kernel(RouteArgs a, int ntiles, int ngroups) {
+  constexpr int TT = R::TT, D = R::D, NB = R::NB, WDMA = R::WDMA;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[D * R::STAGE];
+  __shared__ int s_tau[TT];
   __shared__ int s_first;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // 1-D grid, (token tile, expert group) with the group fastest, XCD-contiguous
-  const int total = ntiles * ngroups;
   const int b = blockIdx.x, xcd = b & 7, j = b >> 3;
-  const int cnt_x = (total >> 3) + (xcd < (total & 7) ? 1 : 0);
-  if (j >= cnt_x) return;
-  const int L = xcd * (total >> 3) + min(xcd, total & 7) + j;
-  const int tile = L / ngroups, grp = L - tile * ngroups;
-  const int t0 = tile * RL_TT;
+  const int lt = j / ngroups, grp = j - lt * ngroups;
+  const int tile = lt * 8 + xcd;
+  if (tile >= ntiles) return;
+  const int t0 = tile * TT;
   const int gpub = (a.n_pub + RL_NE - 1) / RL_NE;
   const int pass = grp < gpub ? 0 : 1;
   const int n0 = (pass ? grp - gpub : grp) * RL_NE;
   const int N = pass ? a.n_priv : a.n_pub;
-  if (tid == 0) s_first = RL_TT;
+  if (tid == 0) s_first = TT;
   __syncthreads();
   int mine = 0;
-  if (tid < RL_TT) {
+  if (tid < TT) {
     const int tau = (t0 + tid < a.T) ? token_tau(a, t0 + tid) : -1;
     s_tau[tid] = tau;
     mine = (a.soft ? tau >= 0 : tau == pass) ? 1 : 0;
@@ -353,11 +363,11 @@ __global__ __launch_bounds__(RL_THREADS) void route_logits_lds_kernel(RouteArgs 
   const int first = s_first;
   auto part = [&](int r) { return a.soft ? s_tau[r] >= 0 : s_tau[r] == pass; };
   // Copy sources, byte offsets from the step's base (x: the tile's first row, so every
-  // offset is below 64 rows of H bf16 whatever T). x: copy jj of wave w fills LDS rows
+  // offset is below TT rows of H bf16 whatever T). x: copy jj of wave w fills LDS rows
   // (2w + jj) * 8 + l / 8, lane l's physical chunk l % 8 holding logical chunk
   // (l % 8) ^ ((row >> 1) & 7); a row whose token has the other policy (or lies past T)
   // copies the tile's first token of this policy, so a token's x is only ever read for
-  // the pool it is permitted. Router: copy jj of wave w fills rows (RL_WDMA w + jj) * 4 +
+  // the pool it is permitted. Router: copy jj of wave w fills rows (WDMA w + jj) * 4 +
   // l / 16, physical chunk l % 16 holding logical chunk (l % 16) ^ (row & 15); rows past
   // the pool copy expert n0 (their results are discarded).
   uint32_t offx[2];
@@ -368,10 +378,10 @@ __global__ __launch_bounds__(RL_THREADS) void route_logits_lds_kernel(RouteArgs 
     const int tok = part(r) ? r : first;  // row within the tile
     offx[jj] = ((uint32_t)tok * (uint32_t)H + c * 8) * 2;
   }
-  uint32_t offw[RL_WDMA];
+  uint32_t offw[WDMA];
 #pragma unroll
-  for (int jj = 0; jj < RL_WDMA; ++jj) {
-    const int r = (RL_WDMA * wave + jj) * 4 + (lane >> 4);
+  for (int jj = 0; jj < WDMA; ++jj) {
+    const int r = (WDMA * wave + jj) * 4 + (lane >> 4);
     const int c = (lane & 15) ^ (r & 15);
     const int n = n0 + r;
     offw[jj] = ((uint32_t)(n < N ? n : n0) * (uint32_t)H + c * 4) * 4;
@@ -383,43 +393,43 @@ __global__ __launch_bounds__(RL_THREADS) void route_logits_lds_kernel(RouteArgs 
   const uint32_t lds0 = lds_addr(smem);
   auto issue = [&](int st) {
     const int kk = ((st + rot) % nsteps) * RL_BK;
-    const uint32_t sx = __builtin_amdgcn_readfirstlane(lds0 + (st % RL_D) * RL_STAGE);
+    const uint32_t sx = __builtin_amdgcn_readfirstlane(lds0 + (st % D) * R::STAGE);
     dma16s<0, false>(offx[0], x + kk, sx + 2 * wave * 1024);
     dma16s<1024, false>(offx[1], x + kk, sx + 2 * wave * 1024);
-    const uint32_t sw = sx + RL_XB + RL_WDMA * wave * 1024;
-    Unroll<0, RL_WDMA>::run([&](auto jj) { dma16s<jj.value * 1024, false>(offw[jj.value], wr + kk, sw); });
+    const uint32_t sw = sx + R::XB + WDMA * wave * 1024;
+    Unroll<0, WDMA>::run([&](auto jj) { dma16s<jj.value * 1024, false>(offw[jj.value], wr + kk, sw); });
   };
   // Fragment addresses within a stage. A: row 16w + (l & 15), 8 bf16 of K sub-step sub at
   // logical chunk 4 sub + l / 16. Router block nb: row 16 nb + (l & 15), the same 8 K
   // values as two fp32 chunks 8 sub + 2 (l / 16) and the next.
   const int ar = wave * 16 + (lane & 15), nr = lane & 15, g = lane >> 4;
-  uint32_t pa[2], pw[RL_NB][2][2];
+  uint32_t pa[2], pw[NB][2][2];
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
     pa[sub] = ar * 128 + (((sub * 4 + g) ^ ((ar >> 1) & 7)) << 4);
 #pragma unroll
-    for (int nb = 0; nb < RL_NB; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
-        pw[nb][sub][h] = RL_XB + (nb * 16 + nr) * 256 + (((sub * 8 + 2 * g + h) ^ nr) << 4);
+        pw[nb][sub][h] = R::XB + (nb * 16 + nr) * 256 + (((sub * 8 + 2 * g + h) ^ nr) << 4);
   }
-  f32x4 acc[RL_NB];
+  f32x4 acc[NB];
 #pragma unroll
-  for (int nb = 0; nb < RL_NB; ++nb) acc[nb] = f32x4{0, 0, 0, 0};
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0, 0, 0, 0};
   int issued = 0;
-  for (; issued < RL_D - 1 && issued < nsteps; ++issued) issue(issued);
+  for (; issued < D - 1 && issued < nsteps; ++issued) issue(issued);
   for (int s = 0; s < nsteps; ++s) {
     // this wave's copies of step s landed (younger steps may stay in flight) ...
-    wait_steps<RL_D - 2>(issued - 1 - s);
+    wait_steps<D - 2, R::NDMA>(issued - 1 - s);
     // ... and every other wave's; every read of step s - 1 is finished
     barrier_raw();
     if (issued < nsteps) issue(issued++);  // into the slot of step s - 1
-    const uint32_t st = (uint32_t)(s % RL_D) * RL_STAGE;
+    const uint32_t st = (uint32_t)(s % D) * R::STAGE;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       const bf16x8 av8 = as_bf16x8(*(const u32x4*)(smem + st + pa[sub]));
 #pragma unroll
-      for (int nb = 0; nb < RL_NB; ++nb) {
+      for (int nb = 0; nb < NB; ++nb) {
         const float4 w0 = *(const float4*)(smem + st + pw[nb][sub][0]);
         const float4 w1 = *(const float4*)(smem + st + pw[nb][sub][1]);
         const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
@@ -441,7 +451,7 @@ __global__ __launch_bounds__(RL_THREADS) void route_logits_lds_kernel(RouteArgs 
   }
   // lane l holds tokens 16w + 4 (l / 16) + i against experts n0 + 16 nb + (l & 15)
 #pragma unroll
-  for (int nb = 0; nb < RL_NB; ++nb)
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int tt = wave * 16 + g * 4 + i;
@@ -501,9 +511,12 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   if (a.act_bf16) {
     if (a.T > 2048) {
-      const int nt = (a.T + RL_TT - 1) / RL_TT;
+      using R = RlLarge;
+      const int nt = (a.T + R::TT - 1) / R::TT;
       const int lgroups = (a.n_pub + RL_NE - 1) / RL_NE + (a.n_priv + RL_NE - 1) / RL_NE;
-      hipLaunchKernelGGL(route_logits_lds_kernel, dim3((nt * lgroups + 7) / 8 * 8), dim3(RL_THREADS), 0, s, a, nt, lgroups);
+      // 8 XCDs x ceil(nt / 8) tiles each x the groups of a tile
+      const int64_t grid = (int64_t)8 * ((nt + 7) / 8) * lgroups;
+      hipLaunchKernelGGL(route_logits_lds_kernel<R>, dim3((unsigned)grid), dim3(R::THREADS), 0, s, a, nt, lgroups);
     } else {
       const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
       const int nt = (a.T + 15) / 16;

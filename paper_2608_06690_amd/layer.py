@@ -205,9 +205,31 @@ class PolicyMaskedMoE:
                            torch.empty(max(N.pmpe_backward_workspace_bytes(d, T), 256),
                                        dtype=torch.uint8, device=dev))
 
+    def _priv_key(self):
+        # identity and torch version counter of the private expert weights: an in-place
+        # torch update or a new tensor changes it (the optimizer's kernel writes through a
+        # raw pointer and refreshes the copies itself)
+        return tuple((w.data_ptr(), w._version) for w in (self.w2_priv, self.w13_priv))
+
+    def refresh_private_transposes(self, stream=None) -> None:
+        """Remake the transposed copies of the private expert weights (after they changed)."""
+        if self.w13_priv is None or self.desc.n_priv == 0:
+            return
+        if getattr(self, "_wt_priv", None) is None:
+            self._wt_priv = (
+                torch.empty(self.w2_priv.shape[0], self.w2_priv.shape[2], self.w2_priv.shape[1],
+                            dtype=self.w2_priv.dtype, device=self.device),
+                torch.empty(self.w13_priv.shape[0], self.w13_priv.shape[2], self.w13_priv.shape[1],
+                            dtype=self.w13_priv.dtype, device=self.device))
+        N.pmpe_transpose_experts(self.w2_priv, self._wt_priv[0], stream)
+        N.pmpe_transpose_experts(self.w13_priv, self._wt_priv[1], stream)
+        self._wt_priv_key = self._priv_key()
+
     def transposed_weights(self, stream=None):
         """Transposed expert weights for the backward: the frozen public ones are made once
-        and kept; the private ones are remade on every call (training changes them)."""
+        and kept; the private ones are made once and remade only when the private weights
+        change (an optimizer step, an in-place torch update or new tensors), not on every
+        backward call."""
         if getattr(self, "_wt_pub", None) is None:
             w2t = torch.empty(self.w2_pub.shape[0], self.w2_pub.shape[2], self.w2_pub.shape[1],
                               dtype=self.w2_pub.dtype, device=self.device)
@@ -218,14 +240,8 @@ class PolicyMaskedMoE:
             self._wt_pub = (w2t, w13t)
         if self.w13_priv is None or self.desc.n_priv == 0:
             return self._wt_pub + (None, None)
-        if getattr(self, "_wt_priv", None) is None:
-            self._wt_priv = (
-                torch.empty(self.w2_priv.shape[0], self.w2_priv.shape[2], self.w2_priv.shape[1],
-                            dtype=self.w2_priv.dtype, device=self.device),
-                torch.empty(self.w13_priv.shape[0], self.w13_priv.shape[2], self.w13_priv.shape[1],
-                            dtype=self.w13_priv.dtype, device=self.device))
-        N.pmpe_transpose_experts(self.w2_priv, self._wt_priv[0], stream)
-        N.pmpe_transpose_experts(self.w13_priv, self._wt_priv[1], stream)
+        if getattr(self, "_wt_priv", None) is None or getattr(self, "_wt_priv_key", None) != self._priv_key():
+            self.refresh_private_transposes(stream)
         return self._wt_pub + self._wt_priv
 
     def backward(self, x, dout, b: LayerBuffers, g: Optional[GradBuffers] = None,
@@ -280,3 +296,7 @@ class PrivateAdamW:
         for p, mp, gr, m, v in zip(self.params, self.master, grads, self.m, self.v):
             N.pmpe_adamw(p, mp, gr, m, v, self.t, self.lr, self.betas[0], self.betas[1], self.eps,
                          self.wd, stream)
+        # the backward's transposed copies of the private experts follow the update (once
+        # per step, on the same stream), if the layer keeps them
+        if getattr(self.layer, "_wt_priv", None) is not None:
+            self.layer.refresh_private_transposes(stream)

@@ -84,3 +84,46 @@ def test_private_training_step_keeps_public_fingerprint():
     assert torch.equal(P.fingerprint_tensors(*pub), fp_pub)
     for before, now in zip(priv_before, (Lw.wr_priv, Lw.w13_priv, Lw.w2_priv)):
         assert not torch.equal(before, now)
+
+
+def test_backward_after_step_uses_the_updated_private_weights():
+    """The transposed private weights are kept between backward calls and remade by the
+    optimizer step: the backward after a step equals the backward of a fresh layer object
+    (which transposes the current weights itself), bitwise, and so does the backward after
+    an in-place torch update of a private weight."""
+    cfg = W.scaled_config(W.get_config("qwen"), tokens=512, requests=4, hidden=256, inter=128,
+                          n_pub=16, n_priv=8, top_k=4)
+    layer, Lw = C.device_layer(cfg)
+    req = W.make_requests(cfg)
+    words = C.words_tensor(O.compile_words(req.metas, req.lengths))
+    x = W.make_x(cfg, "cuda")
+    offs = torch.tensor(req.offsets, device="cuda", dtype=torch.int32)
+    dout = W.make_dout(cfg, device="cuda")
+    opt = P.PrivateAdamW(layer, lr=1e-3)
+
+    def grads(lay):
+        a = lay.audit_buffers(cfg.tokens, len(req.offsets) - 1)
+        b = lay.forward(x, words, a, offs, train=True)
+        g = lay.backward(x, dout, b)
+        torch.cuda.synchronize()
+        return g, [t.clone() for t in (g.dx, g.dw13_priv, g.dw2_priv, g.dwr_priv)]
+
+    def fresh():
+        return P.PolicyMaskedMoE(layer.desc, Lw.wr_pub, Lw.wr_priv, Lw.bias, Lw.w13_pub, Lw.w2_pub,
+                                 Lw.w13_priv, Lw.w2_priv)
+
+    g, _ = grads(layer)
+    opt.step(g)
+    _, after_step = grads(layer)
+    _, ref = grads(fresh())
+    for a, r in zip(after_step, ref):
+        assert torch.equal(a, r)
+    log("  backward after an optimizer step equals a fresh layer's")
+    with torch.no_grad():
+        Lw.w2_priv.mul_(0.5)
+    _, after_edit = grads(layer)
+    _, ref = grads(fresh())
+    for a, r in zip(after_edit, ref):
+        assert torch.equal(a, r)
+    # dW13 and dx flow through W2 (dh = W2^T u); dW2 = u h^T does not
+    assert not torch.equal(after_edit[1], after_step[1]) and not torch.equal(after_edit[0], after_step[0])
