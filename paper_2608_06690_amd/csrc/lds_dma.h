@@ -22,6 +22,12 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // barrier and only then reads the stage they filled. The base and the LDS address are
 // passed through readfirstlane so that they are held in SGPRs whatever the compiler can
 // prove.
+//
+// The assembly must leave SCC alone: the compiler does not know that an asm statement
+// changes it and may place one between its own SCC producer and consumer (the low and
+// high halves of a 64-bit address add, a compare and its branch). So M0 is written with
+// s_mov_b32 (which leaves SCC unchanged) from an LDS address the compiler has already
+// summed, never with s_add_u32.
 __device__ __forceinline__ const void* uniform_ptr(const void* p) {
   const uint64_t v = (uint64_t)(uintptr_t)p;
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
@@ -32,20 +38,20 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
 template <int IMM, bool NT>
 __device__ __forceinline__ void dma16s(uint32_t byte_off, const void* base_, uint32_t lds_base_) {
   const void* base = uniform_ptr(base_);
-  const uint32_t lds_base = __builtin_amdgcn_readfirstlane(lds_base_);
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(lds_base_ + (uint32_t)IMM);
   if constexpr (NT)
     asm volatile(
-        "s_add_u32 m0, %2, %3\n\t"
+        "s_mov_b32 m0, %2\n\t"
         "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, %1 offset:0 nt" ::"v"(byte_off),
-        "s"(base), "s"(lds_base), "n"(IMM)
+        "s"(base), "s"(lds)
         : "memory", "m0");
   else
     asm volatile(
-        "s_add_u32 m0, %2, %3\n\t"
+        "s_mov_b32 m0, %2\n\t"
         "s_nop 0\n\t"
         "global_load_lds_dwordx4 %0, %1 offset:0" ::"v"(byte_off),
-        "s"(base), "s"(lds_base), "n"(IMM)
+        "s"(base), "s"(lds)
         : "memory", "m0");
 }
 
