@@ -151,8 +151,9 @@ pmpe_status pmpe_check_desc(const pmpe_layer_desc* d, int32_t T);
  *   kgap         [T] fp32 out or NULL: k-th minus (k+1)-th largest masked logit,
  *                +inf when the pool has exactly k experts
  *   dev_status   [1] uint32 in/out or NULL: status bits are OR-ed in
- *   ws, ws_bytes workspace (holds the fp32 pool logits), at least
- *                pmpe_workspace_bytes(d, T)
+ *   ws, ws_bytes workspace (holds the fp32 pool logits; for bf16 batches of more than
+ *                2048 tokens up to four partial arrays of a split over H, added in a
+ *                fixed order), at least pmpe_workspace_bytes(d, T)
  */
 pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const float* wr_pub,
                        const float* wr_priv, const float* logit_bias, const uint32_t* policy_word,

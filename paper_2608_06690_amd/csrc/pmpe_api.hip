@@ -57,7 +57,8 @@ int route_zstride(const pmpe_layer_desc* d) {
 }
 
 size_t route_ws(const pmpe_layer_desc* d, int32_t T) {
-  return round_up((size_t)T * route_zstride(d) * 4);
+  const int S = route_ksplit(T, d->hidden, d->n_pub, d->n_priv, d->act_dtype == PMPE_BF16);
+  return round_up((size_t)S * T * route_zstride(d) * 4);
 }
 
 size_t dispatch_ws(const pmpe_layer_desc* d, int32_t T) {
@@ -224,7 +225,8 @@ pmpe_status pmpe_route(const pmpe_layer_desc* d, int32_t T, const void* x, const
   RouteArgs a{T, d->hidden, d->n_pub, d->n_priv, d->top_k, d->gate_mode,
               d->act_dtype == PMPE_BF16, x, wr_pub, wr_priv, logit_bias, policy_word,
               topk_idx, topk_gate, allow, kgap, dev_status, (float*)ws, route_zstride(d),
-              d->route_mode == PMPE_ROUTE_SOFT ? 1 : 0};
+              d->route_mode == PMPE_ROUTE_SOFT ? 1 : 0,
+              route_ksplit(T, d->hidden, d->n_pub, d->n_priv, d->act_dtype == PMPE_BF16)};
   return launched(launch_route(a, (hipStream_t)stream));
 }
 

@@ -92,10 +92,14 @@ struct RouteArgs {
   uint8_t* allow;
   float* kgap;
   uint32_t* dev_status;
-  float* z;     // workspace [T, zstride]: fp32 logits of each token's permitted pool
+  float* z;     // workspace [zsplit, T, zstride]: fp32 logits of each token's permitted pool
   int zstride;
   int soft;     // control arm: every token ranks the concatenated pool (z holds all E logits)
+  int zsplit;   // partial logit arrays (K split of the logits); the top-k adds them in order
 };
+// K splits of the router logits for a batch (1 unless the wide large-batch kernel runs);
+// the route workspace holds this many [T, zstride] fp32 arrays.
+int route_ksplit(int T, int H, int n_pub, int n_priv, int act_bf16);
 hipError_t launch_route(const RouteArgs& a, hipStream_t s);
 
 struct DispatchArgs {

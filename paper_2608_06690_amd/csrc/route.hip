@@ -9,7 +9,8 @@
 //     are discarded, so a deny token's x is never multiplied with a private router row,
 //     and a block with no token of its policy returns before reading its router rows.
 //     Up to 2048 tokens the operands are loaded straight into registers (16-token tiles,
-//     H split across the four waves); larger batches stage them in LDS (64-token tiles).
+//     H split across the four waves); larger batches stage them in LDS (64 tokens x 64
+//     experts, H split across up to four blocks whose partial logits the top-k adds).
 //     bf16 activations: the fp32 router row w is split exactly into three bf16 parts
 //     w = hi + mid + lo (each truncation keeps the next 8 significant bits, so the sum
 //     is exact for normal w); every product x * part is exact in fp32 and the MFMA
@@ -284,36 +285,6 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_bf16_kernel(RouteArgs
   }
 }
 
-// Large batches: token-tile x expert-group logits with both operands staged in LDS.
-// Block (tile, g): TT tokens against RL_NE experts of one pool; wave w owns the tile's
-// 16-token row block w over the whole of H, so no partial sums are exchanged. K steps of
-// 64: a step's x rows (TT x 128 bytes) and fp32 router rows (RL_NE x 256 bytes) are copied
-// whole into a ring of D stages by global->LDS copies, so every request is a full
-// 128-byte line (loads of 64-byte row pieces straight into the MFMA register layout
-// bound the register kernel at this size). The 16-byte chunks of each LDS row are
-// XOR-swizzled by row so that the fragment reads of 16 rows hit distinct banks. Token
-// selection, the exact three-part split, the pool rule and the K rotation are those of
-// the register kernel.
-// 16 experts per block and 6 stages (72 KiB, two blocks per CU): the kernel is bound by the
-// copies in flight per CU, so more concurrent blocks beat fewer re-reads (Qwen-shaped
-// 4096-token batch: 32 experts per block 43 us, 16 experts with 4 stages 38 us, with 6
-// stages 35 us, the register kernel 46 us, top-k included).
-constexpr int RL_NE = 16, RL_BK = 64;
-template <int TT_, int D_>
-struct RlCfg {
-  static constexpr int TT = TT_, D = D_;
-  static constexpr int THREADS = 4 * TT;                 // one wave per 16-token row block
-  static constexpr int WAVES = THREADS / 64;
-  static constexpr int NB = RL_NE / 16;                  // 16-expert blocks per wave
-  static constexpr int XB = TT * RL_BK * 2;              // x bytes per stage
-  static constexpr int WB = RL_NE * RL_BK * 4;           // router bytes per stage
-  static constexpr int STAGE = XB + WB;
-  static constexpr int WDMA = WB / 1024 / WAVES;         // router copies (1 KiB, 4 rows) per wave per stage
-  static constexpr int NDMA = 2 + WDMA;                  // copies per wave per stage: 2 of x, the router's
-  static_assert(TT % 16 == 0 && RL_NE % 16 == 0 && WDMA >= 1 && WDMA * WAVES * 1024 == WB, "router tile");
-};
-using RlLarge = RlCfg<64, 6>;
-
 // Wait for the copies of the oldest step in flight: `younger` steps were issued after it
 // (NDMA copies each, loads complete in order), at most Y of which may stay in flight.
 template <int Y, int NDMA>
@@ -326,32 +297,70 @@ __device__ __forceinline__ void wait_steps(int younger) {
     wait_steps<Y - 1, NDMA>(younger);
 }
 
-// Block b runs on XCD b % 8. Token tiles are dealt round-robin to the XCDs (tile
-// 8 i + x to XCD x) with the groups of one tile adjacent on its XCD, so the blocks
-// that find tokens of their pool spread over all XCDs even when consecutive tiles share
-// a policy (requests are contiguous token ranges), and a tile's x rows are shared in
-// one L2.
+// Large batches, wide tile: 64 tokens x 64 experts of one pool per block. Wave w owns
+// experts n0 + 16 w .. n0 + 16 w + 15 against all 64 tokens (four 16-token row blocks), so
+// each fp32 router value is split into its three bf16 parts by one wave only (a tile of
+// 16 experts whose four waves split H by tokens would split every router value four times)
+// and a tile's x rows are copied once per 64 experts. K steps of BK: the step's x rows
+// (64 x 2BK bytes) and router rows (64 x 4BK bytes) go through a ring of D stages of
+// global->LDS copies, each wave copying the x rows and the router rows of its own 16-row
+// blocks. The K range is split `ksplit` ways: split s writes its partial logits to
+// z + s * T * zstride (split 0 adds the logit bias) and the top-k kernel adds the partials
+// in split order, so the logits are bitwise reproducible. Token selection, the exact
+// three-part split and the pool rule are those of the register kernel above; rows past the pool
+// copy expert n0 and are discarded.
+constexpr int RW_TT = 64, RW_NE = 64, RW_THREADS = 256;
+template <int BK_, int D_>
+struct RwCfg {
+  static constexpr int BK = BK_, D = D_;
+  static constexpr int XR = 2 * BK, WR = 4 * BK;          // bytes per x row, per router row
+  static constexpr int XB = RW_TT * XR, WB = RW_NE * WR;  // bytes per stage
+  static constexpr int STAGE = XB + WB;
+  static constexpr int XC = 16 * XR / 1024, WC = 16 * WR / 1024;  // copies per wave per step
+  static constexpr int XRPC = 1024 / XR, WRPC = 1024 / WR;        // rows per copy
+  static constexpr int NDMA = XC + WC;
+  static constexpr int SUB = BK / 32;                     // MFMA K sub-steps per step
+  static_assert(BK == 32 || BK == 64, "wide router K step");
+  static_assert(RW_TT == 16 * (RW_THREADS / 64) && RW_NE == 16 * (RW_THREADS / 64), "wide router tile");
+};
+using RwLarge = RwCfg<64, 3>;
+
+// Physical 16-byte chunk of logical chunk c in row r, for rows of CPR chunks: XOR-swizzled
+// by row so that the fragment reads of 16 consecutive rows at one logical chunk cover the 64
+// LDS banks once (rows of 64 bytes: four rows per bank line; 128 bytes: two; 256: one).
+template <int CPR>
+__device__ __forceinline__ int rw_swz(int r, int c) {
+  if constexpr (CPR == 4) return c ^ ((r >> 2) & 3);
+  else if constexpr (CPR == 8) return c ^ ((r >> 1) & 7);
+  else return c ^ (r & 15);
+}
+
 template <class R>
-__global__ __launch_bounds__(R::THREADS) void route_logits_lds_kernel(RouteArgs a, int ntiles, int ngroups) {
-  constexpr int TT = R::TT, D = R::D, NB = R::NB, WDMA = R::WDMA;
+__global__ __launch_bounds__(RW_THREADS) void route_logits_wide_kernel(RouteArgs a, int ntiles, int ngroups,
+                                                                      int ksplit) {
+  constexpr int BK = R::BK, D = R::D, CX = R::XR / 16, CW = R::WR / 16;
   __shared__ __attribute__((aligned(16))) unsigned char smem[D * R::STAGE];
-  __shared__ int s_tau[TT];
+  __shared__ int s_tau[RW_TT];
   __shared__ int s_first;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // XCD x = b % 8 takes tiles x, x + 8, ...; on an XCD, block j is (local tile, group,
+  // split) with the split fastest, so the blocks of one tile share its x rows in one L2
   const int b = blockIdx.x, xcd = b & 7, j = b >> 3;
-  const int lt = j / ngroups, grp = j - lt * ngroups;
+  const int per_tile = ngroups * ksplit;
+  const int lt = j / per_tile, rem = j - lt * per_tile;
+  const int grp = rem / ksplit, split = rem - grp * ksplit;
   const int tile = lt * 8 + xcd;
   if (tile >= ntiles) return;
-  const int t0 = tile * TT;
-  const int gpub = (a.n_pub + RL_NE - 1) / RL_NE;
+  const int t0 = tile * RW_TT;
+  const int gpub = (a.n_pub + RW_NE - 1) / RW_NE;
   const int pass = grp < gpub ? 0 : 1;
-  const int n0 = (pass ? grp - gpub : grp) * RL_NE;
+  const int n0 = (pass ? grp - gpub : grp) * RW_NE;
   const int N = pass ? a.n_priv : a.n_pub;
-  if (tid == 0) s_first = TT;
+  if (tid == 0) s_first = RW_TT;
   __syncthreads();
   int mine = 0;
-  if (tid < TT) {
+  if (tid < RW_TT) {
     const int tau = (t0 + tid < a.T) ? token_tau(a, t0 + tid) : -1;
     s_tau[tid] = tau;
     mine = (a.soft ? tau >= 0 : tau == pass) ? 1 : 0;
@@ -362,104 +371,105 @@ __global__ __launch_bounds__(R::THREADS) void route_logits_lds_kernel(RouteArgs 
   const int H = a.H;
   const int first = s_first;
   auto part = [&](int r) { return a.soft ? s_tau[r] >= 0 : s_tau[r] == pass; };
-  // Copy sources, byte offsets from the step's base (x: the tile's first row, so every
-  // offset is below TT rows of H bf16 whatever T). x: copy jj of wave w fills LDS rows
-  // (2w + jj) * 8 + l / 8, lane l's physical chunk l % 8 holding logical chunk
-  // (l % 8) ^ ((row >> 1) & 7); a row whose token has the other policy (or lies past T)
-  // copies the tile's first token of this policy, so a token's x is only ever read for
-  // the pool it is permitted. Router: copy jj of wave w fills rows (WDMA w + jj) * 4 +
-  // l / 16, physical chunk l % 16 holding logical chunk (l % 16) ^ (row & 15); rows past
-  // the pool copy expert n0 (their results are discarded).
-  uint32_t offx[2];
+  // Copy sources as byte offsets from the step's base. x copy jj of wave w fills LDS rows
+  // 16w + XRPC jj + l / CX, lane l's physical chunk l % CX holding logical chunk
+  // rw_swz(row, l % CX); a row whose token has the other policy (or lies past T) copies the
+  // tile's first token of this policy. Router copy jj of wave w fills rows
+  // 16w + WRPC jj + l / CW in the same way.
+  uint32_t offx[R::XC], offw[R::WC];
 #pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
-    const int r = (2 * wave + jj) * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ ((r >> 1) & 7);
-    const int tok = part(r) ? r : first;  // row within the tile
+  for (int jj = 0; jj < R::XC; ++jj) {
+    const int r = 16 * wave + R::XRPC * jj + lane / CX;
+    const int c = rw_swz<CX>(r, lane % CX);
+    const int tok = part(r) ? r : first;
     offx[jj] = ((uint32_t)tok * (uint32_t)H + c * 8) * 2;
   }
-  uint32_t offw[WDMA];
 #pragma unroll
-  for (int jj = 0; jj < WDMA; ++jj) {
-    const int r = (WDMA * wave + jj) * 4 + (lane >> 4);
-    const int c = (lane & 15) ^ (r & 15);
+  for (int jj = 0; jj < R::WC; ++jj) {
+    const int r = 16 * wave + R::WRPC * jj + lane / CW;
+    const int c = rw_swz<CW>(r, lane % CW);
     const int n = n0 + r;
     offw[jj] = ((uint32_t)(n < N ? n : n0) * (uint32_t)H + c * 4) * 4;
   }
   const uint16_t* x = (const uint16_t*)a.x + (size_t)t0 * H;
   const float* wr = pass ? a.wr_priv : a.wr_pub;
-  const int nsteps = H / RL_BK;
-  const int rot = (tile * 5 + grp * 3) % nsteps;  // concurrent blocks read different columns
+  const int ns = H / BK / ksplit;  // K steps of this split
+  const int k0 = split * ns;
+  const int rot = (tile * 5 + grp * 3 + split) % ns;
   const uint32_t lds0 = lds_addr(smem);
   auto issue = [&](int st) {
-    const int kk = ((st + rot) % nsteps) * RL_BK;
+    const int kk = (k0 + (st + rot) % ns) * BK;
     const uint32_t sx = __builtin_amdgcn_readfirstlane(lds0 + (st % D) * R::STAGE);
-    dma16s<0, false>(offx[0], x + kk, sx + 2 * wave * 1024);
-    dma16s<1024, false>(offx[1], x + kk, sx + 2 * wave * 1024);
-    const uint32_t sw = sx + R::XB + WDMA * wave * 1024;
-    Unroll<0, WDMA>::run([&](auto jj) { dma16s<jj.value * 1024, false>(offw[jj.value], wr + kk, sw); });
+    const uint32_t wx = sx + wave * R::XC * 1024, ww = sx + R::XB + wave * R::WC * 1024;
+    Unroll<0, R::XC>::run([&](auto jj) { dma16s<jj.value * 1024, false>(offx[jj.value], x + kk, wx); });
+    Unroll<0, R::WC>::run([&](auto jj) { dma16s<jj.value * 1024, false>(offw[jj.value], wr + kk, ww); });
   };
-  // Fragment addresses within a stage. A: row 16w + (l & 15), 8 bf16 of K sub-step sub at
-  // logical chunk 4 sub + l / 16. Router block nb: row 16 nb + (l & 15), the same 8 K
-  // values as two fp32 chunks 8 sub + 2 (l / 16) and the next.
-  const int ar = wave * 16 + (lane & 15), nr = lane & 15, g = lane >> 4;
-  uint32_t pa[2], pw[NB][2][2];
+  // Fragment addresses within a stage. A (row block mb, sub-step sub): row 16mb + (l&15),
+  // 8 bf16 at logical chunk 4 sub + l/16. Router: row 16w + (l&15), the same 8 K values as
+  // the fp32 chunks 8 sub + 2(l/16) and the next.
+  const int g = lane >> 4, nr = 16 * wave + (lane & 15);
+  uint32_t pa[R::SUB][4], pw[R::SUB][2];
 #pragma unroll
-  for (int sub = 0; sub < 2; ++sub) {
-    pa[sub] = ar * 128 + (((sub * 4 + g) ^ ((ar >> 1) & 7)) << 4);
+  for (int sub = 0; sub < R::SUB; ++sub) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int mb = 0; mb < 4; ++mb) {
+      const int ar = mb * 16 + (lane & 15);
+      pa[sub][mb] = ar * R::XR + (rw_swz<CX>(ar, sub * 4 + g) << 4);
+    }
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-        pw[nb][sub][h] = R::XB + (nb * 16 + nr) * 256 + (((sub * 8 + 2 * g + h) ^ nr) << 4);
+    for (int h = 0; h < 2; ++h) pw[sub][h] = R::XB + nr * R::WR + (rw_swz<CW>(nr, sub * 8 + 2 * g + h) << 4);
   }
-  f32x4 acc[NB];
+  f32x4 acc[4];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0, 0, 0, 0};
+  for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x4{0, 0, 0, 0};
   int issued = 0;
-  for (; issued < D - 1 && issued < nsteps; ++issued) issue(issued);
-  for (int s = 0; s < nsteps; ++s) {
+  for (; issued < D - 1 && issued < ns; ++issued) issue(issued);
+  for (int s = 0; s < ns; ++s) {
     // this wave's copies of step s landed (younger steps may stay in flight) ...
     wait_steps<D - 2, R::NDMA>(issued - 1 - s);
     // ... and every other wave's; every read of step s - 1 is finished
     barrier_raw();
-    if (issued < nsteps) issue(issued++);  // into the slot of step s - 1
+    if (issued < ns) issue(issued++);  // into the slot of step s - 1
     const uint32_t st = (uint32_t)(s % D) * R::STAGE;
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      const bf16x8 av8 = as_bf16x8(*(const u32x4*)(smem + st + pa[sub]));
+    for (int sub = 0; sub < R::SUB; ++sub) {
+      const float4 w0 = *(const float4*)(smem + st + pw[sub][0]);
+      const float4 w1 = *(const float4*)(smem + st + pw[sub][1]);
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+      uint32_t ph[8], pm[8], pl[8];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const float4 w0 = *(const float4*)(smem + st + pw[nb][sub][0]);
-        const float4 w1 = *(const float4*)(smem + st + pw[nb][sub][1]);
-        const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-        uint32_t ph[8], pm[8], pl[8];
+      for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
+      const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
+                                        ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
+      const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
+                                        pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
+      const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
+                                        pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
 #pragma unroll
-        for (int i = 0; i < 8; ++i) split3(wv[i], ph[i], pm[i], pl[i]);
-        const bf16x8 bh = as_bf16x8(u32x4{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16),
-                                          ph[4] | (ph[5] << 16), ph[6] | (ph[7] << 16)});
-        const bf16x8 bm = as_bf16x8(u32x4{pm[0] | (pm[1] << 16), pm[2] | (pm[3] << 16),
-                                          pm[4] | (pm[5] << 16), pm[6] | (pm[7] << 16)});
-        const bf16x8 bl = as_bf16x8(u32x4{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16),
-                                          pl[4] | (pl[5] << 16), pl[6] | (pl[7] << 16)});
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[nb], 0, 0, 0);
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[nb], 0, 0, 0);
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[nb], 0, 0, 0);
+      for (int mb = 0; mb < 4; ++mb) {
+        const bf16x8 av8 = as_bf16x8(*(const u32x4*)(smem + st + pa[sub][mb]));
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bh, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bm, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av8, bl, acc[mb], 0, 0, 0);
       }
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's reads of the slot are done
   }
-  // lane l holds tokens 16w + 4 (l / 16) + i against experts n0 + 16 nb + (l & 15)
+  // lane l holds tokens 16mb + 4(l/16) + i against expert n0 + 16w + (l&15)
+  const int nn = n0 + nr;
+  if (nn >= N) return;
+  float* zp = a.z + (size_t)split * a.T * a.zstride;
+  const float bias = (a.bias && split == 0) ? a.bias[(pass ? a.n_pub : 0) + nn] : 0.0f;
+  const int zc = (a.soft && pass ? a.n_pub : 0) + nn;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+  for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int tt = wave * 16 + g * 4 + i;
-      const int nn = n0 + nb * 16 + nr;
-      if (!part(tt) || nn >= N) continue;
-      float z = acc[nb][i];
-      if (a.bias) z += a.bias[(pass ? a.n_pub : 0) + nn];
-      a.z[(size_t)(t0 + tt) * a.zstride + (a.soft && pass ? a.n_pub : 0) + nn] = z;
+      const int tt = mb * 16 + g * 4 + i;
+      if (!part(tt)) continue;
+      float z = acc[mb][i];
+      if (split == 0 && a.bias) z += bias;
+      zp[(size_t)(t0 + tt) * a.zstride + zc] = z;
     }
 }
 
@@ -486,15 +496,30 @@ __global__ __launch_bounds__(RT_THREADS) void route_logits_f32_kernel(RouteArgs 
   }
 }
 
-// Top-k and gates: one wave per token over its pool's logits.
+// Top-k and gates: one wave per token over its pool's logits. With K-split logits the
+// wave first adds the partial arrays in split order into LDS and ranks that row.
 __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
-  const int t = blockIdx.x * RT_WAVES + (threadIdx.x >> 6);
-  if (t >= a.T) return;
+  __shared__ float s_z[RT_WAVES][2 * PMPE_MAX_POOL];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int t = blockIdx.x * RT_WAVES + w;
+  if (t >= a.T) return;  // wave-uniform; no block barrier follows
   const int tau = token_tau(a, t);
   // masked: the permitted pool; soft (control arm): the concatenated pool
   const int N = a.soft ? a.n_pub + a.n_priv : (tau ? a.n_priv : a.n_pub);
   const int base = (a.soft || !tau) ? 0 : a.n_pub;
   const float* z = a.z + (size_t)t * a.zstride;
+  if (a.zsplit > 1) {
+    const size_t pstride = (size_t)a.T * a.zstride;
+    for (int s = lane; s < N; s += 64) {
+      float v = z[s];
+      for (int p = 1; p < a.zsplit; ++p) v += z[p * pstride + s];
+      s_z[w][s] = v;
+    }
+    // the wave's LDS writes complete before any lane reads another lane's entry
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    __builtin_amdgcn_wave_barrier();
+    z = &s_z[w][0];
+  }
   TopkCtx c{a.T, a.n_pub, a.n_priv, a.k, a.gate_mode, a.topk_idx, a.topk_gate, a.allow, a.kgap};
   if (N <= 64)
     topk_one_token<1>(c, t, tau, N, base, z);
@@ -508,15 +533,27 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
 
 }  // namespace
 
+int route_ksplit(int T, int H, int n_pub, int n_priv, int act_bf16) {
+  if (!act_bf16 || T <= 2048) return 1;
+  // enough blocks to fill the chip (two resident per CU) with the K range of a tile split
+  // over up to four blocks
+  const int64_t nt = (T + RW_TT - 1) / RW_TT;
+  const int64_t groups = (n_pub + RW_NE - 1) / RW_NE + (n_priv + RW_NE - 1) / RW_NE;
+  const int nsteps = H / RwLarge::BK;
+  int S = 1;
+  while (S < 4 && nt * groups * S < 1024 && nsteps % (2 * S) == 0) S *= 2;
+  return S;
+}
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t s) {
   if (a.act_bf16) {
     if (a.T > 2048) {
-      using R = RlLarge;
-      const int nt = (a.T + R::TT - 1) / R::TT;
-      const int lgroups = (a.n_pub + RL_NE - 1) / RL_NE + (a.n_priv + RL_NE - 1) / RL_NE;
-      // 8 XCDs x ceil(nt / 8) tiles each x the groups of a tile
-      const int64_t grid = (int64_t)8 * ((nt + 7) / 8) * lgroups;
-      hipLaunchKernelGGL(route_logits_lds_kernel<R>, dim3((unsigned)grid), dim3(R::THREADS), 0, s, a, nt, lgroups);
+      const int nt = (a.T + RW_TT - 1) / RW_TT;
+      const int groups = (a.n_pub + RW_NE - 1) / RW_NE + (a.n_priv + RW_NE - 1) / RW_NE;
+      // 8 XCDs x ceil(nt / 8) tiles each x the groups and K splits of a tile
+      const int64_t grid = (int64_t)8 * ((nt + 7) / 8) * groups * a.zsplit;
+      hipLaunchKernelGGL(route_logits_wide_kernel<RwLarge>, dim3((unsigned)grid), dim3(RW_THREADS), 0, s, a, nt,
+                         groups, a.zsplit);
     } else {
       const int groups = (a.n_pub + 15) / 16 + (a.n_priv + 15) / 16;
       const int nt = (a.T + 15) / 16;
