@@ -40,18 +40,21 @@ COPY_BYTES = 1 << 30
 
 # HBM traffic of one pmpe_expert_ffn call on the Qwen-shaped layer, from rocprofv3
 # FETCH_SIZE and WRITE_SIZE (summed over its kernels, scaled by the counters' reading
-# for a plain copy of known size). Keyed by the SHA-256 of the kernel source the
-# counters were taken on: any other source reports null.
+# for a plain copy of known size). Keyed by the SHA-256 of the kernel sources the
+# counters were taken on (the GEMM and its copy helper): any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "7b63674b06361163fc6430fb1615ce68724240b739db14f7da767a0b81ddb6fe": 1_985_500_173,
+    "f85167b97d3ea9b7fab88d6146c1e69feebffa462965066a7193834102e71ba4": 2_021_455_959,
 }
+FFN_SOURCES = ("ffn.hip", "lds_dma.h")
 
 
 def ffn_source_hash():
     import hashlib
-    path = os.path.join(ROOT, "paper_2608_06690_amd", "csrc", "ffn.hip")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for name in FFN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_06690_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def parse():
