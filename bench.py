@@ -92,6 +92,9 @@ def parse():
                    help="time only the DeepSeek-V2-Lite-shaped layer (for a separate kernel profile)")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="run only a plain 1 GiB device-to-device copy (counter calibration)")
+    p.add_argument("--read-probe", action="store_true",
+                   help="time only torch reductions that stream 0.9 GB from HBM once, L2/MALL "
+                        "flushed before each (context for the decode rate: a plain read stream)")
     return p.parse_args()
 
 
@@ -587,6 +590,29 @@ def main():
         ms = e0.elapsed_time(e1) / 5
         print(json.dumps({"copy_bytes": COPY_BYTES, "copy_us": ms * 1e3,
                           "read_plus_write_gbs": 2 * COPY_BYTES / (ms * 1e-3) / 1e9}), flush=True)
+        return
+    if args.read_probe:
+        # the decode workload's weight volume (96 experts x 9,437,184 bytes), read once
+        nbytes = 96 * 3 * 2048 * 768 * 2
+        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        out = {"bytes": nbytes}
+        for name, fn in (("sum_bf16", lambda: src.sum(dtype=torch.float32)),
+                         ("amax_bf16", lambda: src.amax())):
+            ts = []
+            for i in range(8):
+                flush.fill_(1)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                if i >= 2:
+                    ts.append(e0.elapsed_time(e1) * 1e3)
+            us = sorted(ts)[len(ts) // 2]
+            out[name] = {"us_median": us, "gbs": nbytes / (us * 1e-6) / 1e9,
+                         "hbm_frac": nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+        print(json.dumps(out), flush=True)
         return
     if args.decode_only:
         print(json.dumps(decode_bench(args, dev)), flush=True)
