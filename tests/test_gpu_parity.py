@@ -110,6 +110,8 @@ LARGE_ROUTE = [
     dict(tokens=2049, requests=7, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),  # one-token last tile
     dict(tokens=2113, requests=9, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),
     dict(tokens=4100, requests=5, hidden=384, inter=128, n_pub=128, n_priv=32, top_k=8),
+    # both pools over several partly filled 64-expert groups, H split four ways
+    dict(tokens=2500, requests=5, hidden=512, inter=128, n_pub=100, n_priv=70, top_k=6),
 ]
 
 

@@ -66,7 +66,8 @@ def test_soft_router_tiny_fp32():
     dict(tokens=200, requests=4, hidden=256, inter=128, n_pub=200, n_priv=100, top_k=8),  # pool of 300
     # above 2048 tokens: the LDS-staged router, a ragged last tile, mixed-policy tiles
     dict(tokens=2150, requests=5, hidden=256, inter=128, n_pub=40, n_priv=12, top_k=4),
-], ids=["E36", "E300", "T2150"])
+    dict(tokens=2200, requests=4, hidden=256, inter=128, n_pub=200, n_priv=100, top_k=8),  # pool of 300, large batch
+], ids=["E36", "E300", "T2150", "T2200_E300"])
 def test_soft_router_small_bf16_leaks_and_is_audited(shape):
     cfg = W.scaled_config(W.get_config("qwen"), **shape)
     req = W.alternating_requests(cfg.requests, cfg.tokens // cfg.requests)
