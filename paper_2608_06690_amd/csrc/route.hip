@@ -50,6 +50,24 @@ __device__ __forceinline__ void split3(float w, uint32_t& h, uint32_t& m, uint32
   l = __float_as_uint(r2) >> 16;
 }
 
+// The value of lane (lane ^ stride) for the strides of a wave bitonic network, without the
+// LDS crossbar where a lane-permuting move does it: DPP quad permutations for strides 1 and 2,
+// a rotation by 8 within each row of 16 lanes for stride 8 (a rotation by 8 of 16 lanes is
+// the xor), ds_swizzle (xor mask within 32 lanes) for 4 and 16, a full shuffle for 32.
+__device__ __forceinline__ uint32_t xor_lanes(uint32_t x, int stride) {
+  const int v = (int)x;
+  if (stride == 1) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);  // [1,0,3,2]
+  if (stride == 2) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);  // [2,3,0,1]
+  if (stride == 8) return (uint32_t)__builtin_amdgcn_mov_dpp(v, 0x128, 0xF, 0xF, false);  // row_ror:8
+  if (stride == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle(v, (4 << 10) | 0x1F);
+  if (stride == 16) return (uint32_t)__builtin_amdgcn_ds_swizzle(v, (16 << 10) | 0x1F);
+  return (uint32_t)__shfl_xor(v, stride, 64);
+}
+__device__ __forceinline__ uint64_t xor_lanes_u64(uint64_t v, int stride) {
+  const uint32_t lo = xor_lanes((uint32_t)v, stride), hi = xor_lanes((uint32_t)(v >> 32), stride);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 // Bitonic sort (ascending) of NPL*64 keys held NPL per lane; element i = r*64 + lane.
 template <int NPL>
 __device__ __forceinline__ void wave_bitonic_sort(uint64_t (&v)[NPL]) {
@@ -75,7 +93,7 @@ __device__ __forceinline__ void wave_bitonic_sort(uint64_t (&v)[NPL]) {
       } else {
 #pragma unroll
         for (int r = 0; r < NPL; ++r) {
-          const uint64_t o = shfl_xor_u64(v[r], stride);
+          const uint64_t o = xor_lanes_u64(v[r], stride);
           const bool asc = (((r << 6) | lane) & size) == 0;
           const bool lower = (lane & stride) == 0;
           const uint64_t mn = v[r] < o ? v[r] : o;
