@@ -43,7 +43,7 @@ constexpr int MAXG = 2 * PMPE_MAX_POOL;
 // Per-token row pass
 // ---------------------------------------------------------------------------
 // Block t: dg_j = G_t . y_perm[r_j] (fixed-order block reduction), dz_j (RENORM),
-// dY[r_j] = bf16(g_j G_t), Xp[r_j] = x_t, dz_row[r_j] = dz_j.
+// dY[r_j] = bf16(g_j G_t), Xp[r_j] = x_t (when a later pass reads it), dz_row[r_j] = dz_j.
 __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
   __shared__ float s_part[BT / 64][PMPE_MAX_TOPK];
   __shared__ float s_dz[PMPE_MAX_TOPK];
@@ -65,15 +65,24 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
       gf[2 * q] = bf16_to_f32(gv[q] & 0xFFFFu);
       gf[2 * q + 1] = bf16_to_f32(gv[q] >> 16);
     }
+    // eight rows' loads at a time, unconditional (slots past k reload slot k - 1, unused)
 #pragma unroll
-    for (int j = 0; j < PMPE_MAX_TOPK; ++j) {
-      if (j < k) {
-        const u32x4 yv = *(const u32x4*)(y + (size_t)s_row[j] * H + c * 8);
-        float s = 0.f;
+    for (int j0 = 0; j0 < PMPE_MAX_TOPK; j0 += 8) {
+      if (j0 < k) {
+        u32x4 yv[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          s += gf[2 * q] * bf16_to_f32(yv[q] & 0xFFFFu) + gf[2 * q + 1] * bf16_to_f32(yv[q] >> 16);
-        part[j] += s;
+        for (int jj = 0; jj < 8; ++jj)
+          yv[jj] = __builtin_nontemporal_load((const u32x4*)(y + (size_t)s_row[min(j0 + jj, k - 1)] * H + c * 8));
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          if (j0 + jj < k) {
+            float s = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              s += gf[2 * q] * bf16_to_f32(yv[jj][q] & 0xFFFFu) + gf[2 * q + 1] * bf16_to_f32(yv[jj][q] >> 16);
+            part[j0 + jj] += s;
+          }
+        }
       }
     }
   }
@@ -101,6 +110,9 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
   __syncthreads();
   if (tid < k) a.dz_row[s_row[tid]] = s_dz[tid];
   const uint16_t* xt = (const uint16_t*)a.x + (size_t)t * H;
+  // the gathered copy of x feeds the recomputed [a; b] and the transposing weight-gradient
+  // GEMM; the K-contiguous private copies gather x by token themselves
+  const bool need_xp = a.ab == nullptr || (a.n_priv > 0 && a.tr == nullptr);
   for (int c = tid; c < nch; c += BT) {
     const u32x4 gv = *(const u32x4*)(G + c * 8);
     const u32x4 xv = *(const u32x4*)(xt + c * 8);
@@ -112,7 +124,7 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
         o[q] = pack_bf16x2(g * bf16_to_f32(gv[q] & 0xFFFFu), g * bf16_to_f32(gv[q] >> 16));
       const size_t r = (size_t)s_row[j];
       *(u32x4*)(a.dY + r * H + c * 8) = o;
-      *(u32x4*)(a.Xp + r * H + c * 8) = xv;
+      if (need_xp) *(u32x4*)(a.Xp + r * H + c * 8) = xv;
     }
   }
 }
@@ -359,9 +371,12 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
 // ---------------------------------------------------------------------------
 // SwiGLU backward on the rows of dh (NT path): da = dh b s (1 + a (1 - s)),
 // db = dh a s, h = a s b, with [a; b] the saved fp32 gate and up projections; four
-// columns per thread.
-__global__ __launch_bounds__(BT) void bwd_swiglu_kernel(BwdArgs a, const float* AB) {
+// columns per thread. With pub_only, block r stops at the first private row (the private
+// rows' tile pass writes theirs together with their K-contiguous copies) and h is not
+// written (only the private experts' weight gradients read it).
+__global__ __launch_bounds__(BT) void bwd_swiglu_kernel(BwdArgs a, const float* AB, int pub_only) {
   const int r = blockIdx.x, I = a.I;
+  if (pub_only && r >= a.offset[a.n_pub]) return;
   const uint16_t* dh = a.dH + (size_t)r * I;
   const float* ab = AB + (size_t)r * 2 * I;
   uint16_t* da = a.dA13 + (size_t)r * 2 * I;
@@ -372,16 +387,11 @@ __global__ __launch_bounds__(BT) void bwd_swiglu_kernel(BwdArgs a, const float* 
     const f32x4 g = *(const f32x4*)(ab + i), u = *(const f32x4*)(ab + I + i);
     float dga[4], dub[4], h[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float d = bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu);
-      const float s = 1.0f / (1.0f + __expf(-g[j]));
-      dga[j] = d * u[j] * s * (1.0f + g[j] * (1.0f - s));
-      dub[j] = d * g[j] * s;
-      h[j] = g[j] * s * u[j];
-    }
+    for (int j = 0; j < 4; ++j)
+      swiglu_bwd(bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu), g[j], u[j], dga[j], dub[j], h[j]);
     *(u32x2*)(da + i) = u32x2{pack_bf16x2(dga[0], dga[1]), pack_bf16x2(dga[2], dga[3])};
     *(u32x2*)(da + I + i) = u32x2{pack_bf16x2(dub[0], dub[1]), pack_bf16x2(dub[2], dub[3])};
-    *(u32x2*)(hh + i) = u32x2{pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3])};
+    if (!pub_only) *(u32x2*)(hh + i) = u32x2{pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3])};
   }
 }
 
@@ -439,49 +449,80 @@ __global__ __launch_bounds__(BT) void bwd_pool_dz_kernel(BwdArgs a) {
   }
 }
 
-// dx_t = sum_j dXr[r_j] (slot order) + router term + shared-expert term, four columns per
-// thread. Router term: RENORM sum_j dz_j W_r[e_j]; POOL_SOFTMAX sum over the pool of
-// dz_e W_r[e] in id order.
+// dx_t = sum_j dXr[r_j] (slot order) + router term + shared-expert term, eight columns per
+// thread (the k rows' loads are all issued before the ordered sum). Router term: RENORM
+// sum_j dz_j W_r[e_j]; POOL_SOFTMAX sum over the pool of dz_e W_r[e] in id order.
+template <bool NT>  // NT: bf16 row input gradients (the NT path), else fp32
 __global__ __launch_bounds__(BT) void bwd_dx_kernel(BwdArgs a) {
   __shared__ int s_r[PMPE_MAX_TOPK];
-  __shared__ const float* s_w[PMPE_MAX_TOPK];
+  __shared__ int s_e[PMPE_MAX_TOPK];
   __shared__ float s_dz[PMPE_MAX_TOPK];
   const int t = blockIdx.x, H = a.H, k = a.k, tid = threadIdx.x;
   if (tid < k) {
-    const int r = a.token_row[t * k + tid], e = a.topk_idx[t * k + tid];
+    const int r = a.token_row[t * k + tid];
     s_r[tid] = r;
+    s_e[tid] = a.topk_idx[t * k + tid];
     s_dz[tid] = a.pool_gates ? 0.f : a.dz_row[r];
-    s_w[tid] = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
   }
   __syncthreads();
   const bool priv = a.topk_idx[t * k] >= a.n_pub;
   const int first = a.soft ? 0 : (priv ? a.n_pub : 0);
   const int pool = a.soft ? a.n_pub + a.n_priv : (priv ? a.n_priv : a.n_pub);
   const float* dzp = a.pool_gates ? a.dz_pool + (size_t)t * a.pool_stride : nullptr;
-  for (int h = tid * 4; h < H; h += BT * 4) {
-    f32x4 s = {0, 0, 0, 0};
-    for (int j = 0; j < k; ++j) {
-      f32x4 d;
-      if (a.w2t_pub) {  // NT path: bf16 row input gradients
-        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-        const u32x2 v = *(const u32x2*)((const uint16_t*)a.dXr + (size_t)s_r[j] * H + h);
-        d = f32x4{bf16_to_f32(v[0] & 0xFFFFu), bf16_to_f32(v[0] >> 16), bf16_to_f32(v[1] & 0xFFFFu),
-                  bf16_to_f32(v[1] >> 16)};
-      } else {
-        d = *(const f32x4*)(a.dXr + (size_t)s_r[j] * H + h);
+  for (int h = tid * 8; h < H; h += BT * 8) {
+    f32x4 s[2] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
+    // up to eight rows in flight, summed in slot order. The slots' rows, experts and dz are
+    // read from LDS before any global load (an LDS read waits for every older LDS-counted
+    // operation), the router rows are addressed from the kernel's own global pointers, and
+    // the loads are unconditional (slots past k reload slot k - 1 and are not added).
+    for (int j0 = 0; j0 < k; j0 += 8) {
+      int rj[8], ej[8];
+      float dzj[8];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        const int j = min(j0 + jj, k - 1);
+        rj[jj] = s_r[j];
+        ej[jj] = s_e[j];
+        dzj[jj] = s_dz[j];
       }
-      const f32x4 w = *(const f32x4*)(s_w[j] + h);
-      s += d + s_dz[j] * w;
-    }
-    if (dzp) {
-      for (int i = 0; i < pool; ++i) {
-        const int e = first + i;
-        const float* w = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
-        s += dzp[i] * *(const f32x4*)(w + h);
+      f32x4 d[8][2], w[8][2];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if constexpr (NT) {
+          // read once: keep the L2 for the router rows that every token re-reads
+          const u32x4 v = __builtin_nontemporal_load((const u32x4*)((const uint16_t*)a.dXr + (size_t)rj[jj] * H + h));
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+            d[jj][q] = f32x4{bf16_to_f32(v[2 * q] & 0xFFFFu), bf16_to_f32(v[2 * q] >> 16),
+                             bf16_to_f32(v[2 * q + 1] & 0xFFFFu), bf16_to_f32(v[2 * q + 1] >> 16)};
+        } else {
+          d[jj][0] = *(const f32x4*)(a.dXr + (size_t)rj[jj] * H + h);
+          d[jj][1] = *(const f32x4*)(a.dXr + (size_t)rj[jj] * H + h + 4);
+        }
+        const int e = ej[jj];
+        const float* wr = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
+        w[jj][0] = *(const f32x4*)(wr + h);
+        w[jj][1] = *(const f32x4*)(wr + h + 4);
+      }
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (j0 + jj < k) {
+#pragma unroll
+          for (int q = 0; q < 2; ++q) s[q] += d[jj][q] + dzj[jj] * w[jj][q];
+        }
       }
     }
-    if (a.dXsh) s += *(const f32x4*)(a.dXsh + (size_t)t * H + h);
-    *(f32x4*)(a.dx + (size_t)t * H + h) = s;
+    for (int i = 0; dzp && i < pool; ++i) {
+      const int e = first + i;
+      const float* w = e < a.n_pub ? a.wr_pub + (size_t)e * H : a.wr_priv + (size_t)(e - a.n_pub) * H;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) s[q] += dzp[i] * *(const f32x4*)(w + h + 4 * q);
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      if (a.dXsh) s[q] += *(const f32x4*)(a.dXsh + (size_t)t * H + h + 4 * q);
+      *(f32x4*)(a.dx + (size_t)t * H + h + 4 * q) = s[q];
+    }
   }
 }
 
@@ -514,7 +555,7 @@ __global__ __launch_bounds__(BT) void bwd_dwr_pool_part_kernel(BwdArgs a) {
 }
 
 // Router-row gradient of private expert p, in two fixed-order stages: block (p, c) sums
-// dz_r Xp[r] over the c-th of BWD_DWR_SPLIT equal chunks of p's rows (ascending), eight
+// dz_r x[token of r] over the c-th of BWD_DWR_SPLIT equal chunks of p's rows (ascending), eight
 // columns per thread; then dW_r[p] = sum over the chunks in order. grad_rows[p] = rows.
 __global__ __launch_bounds__(BT) void bwd_dwr_part_kernel(BwdArgs a) {
   const int pe = blockIdx.x, c = blockIdx.y, e = a.n_pub + pe, H = a.H;
@@ -523,15 +564,28 @@ __global__ __launch_bounds__(BT) void bwd_dwr_part_kernel(BwdArgs a) {
   const int per = (cnt + BWD_DWR_SPLIT - 1) / BWD_DWR_SPLIT;
   const int r0 = off + min(cnt, c * per), r1 = off + min(cnt, (c + 1) * per);
   float* part = a.dwr_part + ((size_t)pe * BWD_DWR_SPLIT + c) * H;
+  const uint16_t* x = (const uint16_t*)a.x;
   for (int h = threadIdx.x * 8; h < H; h += BT * 8) {
     float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int r = r0; r < r1; ++r) {
-      const u32x4 v = *(const u32x4*)(a.Xp + (size_t)r * H + h);
-      const float dz = a.dz_row[r];
+    // eight rows' loads in flight (rows past r1 reload row r1 - 1 and are not added)
+    for (int rb = r0; rb < r1; rb += 8) {
+      u32x4 v[8];
+      float dz[8];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        s[2 * q] += dz * bf16_to_f32(v[q] & 0xFFFFu);
-        s[2 * q + 1] += dz * bf16_to_f32(v[q] >> 16);
+      for (int i = 0; i < 8; ++i) {
+        const int r = min(rb + i, r1 - 1);
+        dz[i] = a.dz_row[r];
+        v[i] = *(const u32x4*)(x + (size_t)a.row_token[r] * H + h);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (rb + i < r1) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            s[2 * q] += dz[i] * bf16_to_f32(v[i][q] & 0xFFFFu);
+            s[2 * q + 1] += dz[i] * bf16_to_f32(v[i][q] >> 16);
+          }
+        }
       }
     }
     *(f32x4*)(part + h) = f32x4{s[0], s[1], s[2], s[3]};
@@ -625,8 +679,14 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     f.y_perm = a.dH;
     e = launch_grouped_nt_gemm(f, s);
     if (e != hipSuccess) return e;
-    bwd_swiglu_kernel<<<R, BT, 0, s>>>(a, AB);
+    // with K-contiguous private copies, the private rows go through the tile pass that
+    // also writes [da; db] and h transposed for the weight gradients
+    const bool priv_t = a.n_priv > 0 && a.tr;
+    bwd_swiglu_kernel<<<R, BT, 0, s>>>(a, AB, priv_t ? 1 : 0);
     e = hipGetLastError();
+    if (e == hipSuccess && priv_t)
+      e = launch_swiglu_priv_t(a.dH, AB, a.dA13, a.tr, a.tr + (size_t)2 * I * a.P, R, I, a.P, a.count,
+                               a.offset, a.n_pub, a.n_priv, s);
     if (e != hipSuccess) return e;
     f.H = H; f.I = 2 * I;  // N = H, K = 2I
     f.w13_pub = f.w2_pub = a.w13t_pub;
@@ -654,20 +714,23 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
   }
   if (a.n_priv > 0 && a.tr) {
     // K-contiguous copies of the private rows (zero-padded per expert to multiples of 64),
-    // then the weight gradients on MFMA with 256 x 256 tiles; the copies of one product
-    // are dead once it has run, so the next product reuses the region
-    // dW2[p] = dY^T Hh over private expert p's rows: M = H, N = I
-    uint16_t* at = a.tr;
-    uint16_t* bt = a.tr + (size_t)H * a.P;
-    e = launch_transpose_priv(a.dY, at, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
-    if (e == hipSuccess) e = launch_transpose_priv(a.Hh, bt, R, I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
-    if (e == hipSuccess) e = launch_wgrad(WgradArgs{H, I, a.P, a.n_pub, a.n_priv, at, bt, a.count, a.dw2_priv}, s);
-    if (e != hipSuccess) return e;
-    // dW13[p] = [da; db]^T Xp: M = 2I, N = H
-    bt = a.tr + (size_t)2 * I * a.P;
-    e = launch_transpose_priv(a.dA13, at, R, 2 * I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
-    if (e == hipSuccess) e = launch_transpose_priv(a.Xp, bt, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
-    if (e == hipSuccess) e = launch_wgrad(WgradArgs{2 * I, H, a.P, a.n_pub, a.n_priv, at, bt, a.count, a.dw13_priv}, s);
+    // then the weight gradients on MFMA with 256 x 256 tiles. Regions of tr: [da; db]^T
+    // [2I, P], h^T [I, P] (both written by the private SwiGLU tile pass on the NT path),
+    // and one [H, P] region that holds x^T for dW13 and then dY^T for dW2.
+    uint16_t* daT = a.tr;
+    uint16_t* hT = a.tr + (size_t)2 * I * a.P;
+    uint16_t* cT = a.tr + (size_t)3 * I * a.P;
+    if (!a.w2t_pub) {
+      e = launch_transpose_priv(a.dA13, nullptr, daT, R, 2 * I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+      if (e == hipSuccess) e = launch_transpose_priv(a.Hh, nullptr, hT, R, I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+      if (e != hipSuccess) return e;
+    }
+    // dW13[p] = [da; db]^T X over private expert p's rows (x gathered by token): M = 2I, N = H
+    e = launch_transpose_priv(a.x, a.row_token, cT, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    if (e == hipSuccess) e = launch_wgrad(WgradArgs{2 * I, H, a.P, a.n_pub, a.n_priv, daT, cT, a.count, a.dw13_priv}, s);
+    // dW2[p] = dY^T h: M = H, N = I
+    if (e == hipSuccess) e = launch_transpose_priv(a.dY, nullptr, cT, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    if (e == hipSuccess) e = launch_wgrad(WgradArgs{H, I, a.P, a.n_pub, a.n_priv, cT, hT, a.count, a.dw2_priv}, s);
     if (e != hipSuccess) return e;
   } else if (a.n_priv > 0) {
     // dW2[p] = dY^T Hh over private expert p's rows: M = H, N = I
@@ -695,7 +758,10 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  bwd_dx_kernel<<<a.T, BT, 0, s>>>(a);
+  if (a.w2t_pub)
+    bwd_dx_kernel<true><<<a.T, BT, 0, s>>>(a);
+  else
+    bwd_dx_kernel<false><<<a.T, BT, 0, s>>>(a);
   return hipGetLastError();
 }
 

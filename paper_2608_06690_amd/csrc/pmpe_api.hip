@@ -101,15 +101,16 @@ BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
   L.dash = o; o += round_up(Tt * 2 * Is * 2);
   L.dxsh = o; o += Is > 0 ? round_up(Tt * H * 4) : 0;
   L.dh = o; o += round_up(R * I * 2);
-  // private rows transposed and padded per expert: [max(2I + H, H + I), P] bf16, used when
-  // every byte offset of the weight-gradient copies fits in 31 bits
+  // private rows transposed and padded per expert: [3I + H, P] bf16 ([da; db], h, and one
+  // region for x and then dY), used when every byte offset of the weight-gradient copies
+  // fits in 31 bits
   const size_t P = (R + 63) / 64 * 64 + 64 * (size_t)d->n_priv;
   const size_t wmax = 2 * I > H ? 2 * I : H;
   L.P = 0;
   L.tr = o;
   if (d->n_priv > 0 && wmax * P * 2 < ((size_t)1 << 31)) {
     L.P = (int)P;
-    o += round_up((2 * I + H) * P * 2);
+    o += round_up((3 * I + H) * P * 2);
   }
   L.total = o;
   return L;

@@ -38,6 +38,15 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
+// SwiGLU backward of one element: upstream d = dL/dh, gate projection g, up projection u;
+// h = silu(g) u, da = d u s (1 + g (1 - s)), db = d g s with s = sigmoid(g).
+__device__ __forceinline__ void swiglu_bwd(float d, float g, float u, float& da, float& db, float& h) {
+  const float s = 1.0f / (1.0f + __expf(-g));
+  da = d * u * s * (1.0f + g * (1.0f - s));
+  db = d * g * s;
+  h = g * s * u;
+}
+
 // Wave-level helpers (wave64).
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
@@ -265,7 +274,7 @@ struct BwdArgs {
   const void* w2t_priv;
   const void* w13t_priv;
   uint16_t* dH;           // [T*k, I] bf16 (NT path)
-  // private rows transposed and padded per expert ([max(2I + H, H + I), P] bf16), or NULL:
+  // private rows transposed and padded per expert ([3I + H, P] bf16), or NULL:
   // the weight gradients then run on the transposing GEMM
   uint16_t* tr;
   int P;
@@ -274,9 +283,17 @@ constexpr int BWD_DWR_SPLIT = 16;  // row chunks per private expert in the route
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t s);
 hipError_t launch_transpose(const void* src, void* dst, int n, int rows, int cols, hipStream_t s);
-hipError_t launch_transpose_priv(const void* src, void* dst, int rows_max, int cols, int P,
-                                 const int32_t* count, const int32_t* offset, int n_pub,
-                                 int n_priv, hipStream_t s);
+// dst [cols, P]: the private rows of src transposed and zero-padded per expert (src [rows,
+// cols] in permuted row order, or [T, cols] read through row_token when that is not NULL).
+hipError_t launch_transpose_priv(const void* src, const int32_t* row_token, void* dst, int rows_max,
+                                 int cols, int P, const int32_t* count, const int32_t* offset,
+                                 int n_pub, int n_priv, hipStream_t s);
+// SwiGLU backward of the private rows of dH [rows, I] with [a; b] from AB [rows, 2I]: [da; db]
+// into dA13 [rows, 2I] and, transposed and padded like launch_transpose_priv, into daT
+// [2I, P]; h into hT [I, P].
+hipError_t launch_swiglu_priv_t(const uint16_t* dH, const float* AB, uint16_t* dA13, uint16_t* daT,
+                                uint16_t* hT, int rows_max, int I, int P, const int32_t* count,
+                                const int32_t* offset, int n_pub, int n_priv, hipStream_t s);
 
 // Weight gradients of the private experts on MFMA from K-contiguous operands:
 // C[p] [M, N] fp32 = sum over the padded rows j of private expert p of AT[m][po_p + j] *
