@@ -470,7 +470,9 @@ pmpe_status pmpe_cache_tag_check(const pmpe_cache_tag* cache, const pmpe_cache_t
  *   grad_rows [n_priv] uint32 out or NULL       rows that entered each private
  *                                               expert's gradient
  *   ws                                          pmpe_backward_workspace_bytes(d, T)
- *                                               bytes, 16-byte aligned
+ *                                               bytes
+ * x, dout, y_perm, every weight array, ab, ws, dx and the three gradient outputs are
+ * 16-byte aligned (dx is written in 16-byte vectors).
  *
  * Errors: PMPE_ERR_DTYPE (not bf16), PMPE_ERR_SHAPE (inter or the shared width not a
  * multiple of 128), PMPE_ERR_NULL, PMPE_ERR_ALIGN, PMPE_ERR_WORKSPACE.

@@ -451,7 +451,7 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
   if (any_t && (!w2t_pub || !w13t_pub || (d->n_priv > 0 && (!w2t_priv || !w13t_priv))))
     return PMPE_ERR_NULL;
   const void* al[] = {x, dout, y_perm, w13_pub, w2_pub, w13_priv, w2_priv, ab, w13_sh, w2_sh,
-                      w2t_pub, w13t_pub, w2t_priv, w13t_priv};
+                      w2t_pub, w13t_pub, w2t_priv, w13t_priv, dx, dw13_priv, dw2_priv, dwr_priv};
   for (const void* p : al)
     if (p && !aligned16(p)) return PMPE_ERR_ALIGN;
   if (T == 0) return PMPE_OK;

@@ -151,6 +151,26 @@ def test_null_and_alignment_rejected_before_launch():
     assert st == -2
 
 
+def test_backward_rejects_misaligned_outputs_before_launch():
+    """A misaligned dx or gradient array is refused (PMPE_ERR_ALIGN) before any launch
+    (dx is written in 16-byte vectors)."""
+    d = desc()
+    assert d.act_dtype == P.PMPE_BF16
+    lib = N.lib()
+
+    def call(dx=0x20000, dw13=0x21000, dw2=0x22000, dwr=0x23000):
+        # x dout idx gate count offset row_token token_row y_perm wr_pub wr_priv w13_pub w2_pub
+        # w13_priv w2_priv bias w13_sh w2_sh w2t_pub w13t_pub w2t_priv w13t_priv ab
+        ins = [0x1000 * (i + 1) for i in range(15)] + [None, None, None, None, None, None, None, None]
+        return lib.pmpe_backward(ctypes.byref(d), 16, *ins, dx, dw13, dw2, dwr, None, 0x30000, 1 << 30, None)
+
+    assert call(dx=0x20004) == -5
+    assert call(dw13=0x21008) == -5
+    assert call(dw2=0x22004) == -5
+    assert call(dwr=0x2300C) == -5
+    assert call(dx=None) == -1
+
+
 def test_fingerprint_workspace_and_validation():
     lib = N.lib()
     ws = P.pmpe_fingerprint_workspace_bytes
