@@ -43,7 +43,8 @@ constexpr int MAXG = 2 * PMPE_MAX_POOL;
 // Per-token row pass
 // ---------------------------------------------------------------------------
 // Block t: dg_j = G_t . y_perm[r_j] (fixed-order block reduction), dz_j (RENORM),
-// dY[r_j] = bf16(g_j G_t), Xp[r_j] = x_t (when a later pass reads it), dz_row[r_j] = dz_j.
+// dY[r_j] = bf16(g_j G_t) and Xp[r_j] = x_t (when a later pass reads them), dz_row[r_j] = dz_j,
+// g_row[r_j] = g_j.
 __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
   __shared__ float s_part[BT / 64][PMPE_MAX_TOPK];
   __shared__ float s_dz[PMPE_MAX_TOPK];
@@ -108,11 +109,18 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
     for (int j = 0; j < k; ++j) s_dz[j] = a.pool_gates ? dg[j] : g[j] * (dg[j] - sum);
   }
   __syncthreads();
-  if (tid < k) a.dz_row[s_row[tid]] = s_dz[tid];
+  if (tid < k) {
+    a.dz_row[s_row[tid]] = s_dz[tid];
+    a.g_row[s_row[tid]] = a.topk_gate[t * k + tid];
+  }
   const uint16_t* xt = (const uint16_t*)a.x + (size_t)t * H;
-  // the gathered copy of x feeds the recomputed [a; b] and the transposing weight-gradient
-  // GEMM; the K-contiguous private copies gather x by token themselves
+  // The gathered copy of x feeds the recomputed [a; b] and the transposing weight-gradient
+  // GEMM; the K-contiguous private copies gather x by token themselves. The scaled rows dY
+  // feed the transposing GEMMs only: on the NT path dh gathers dout by token (its rows are
+  // scaled by g_row in the SwiGLU pass) and the K-contiguous private dY is made from dout.
   const bool need_xp = a.ab == nullptr || (a.n_priv > 0 && a.tr == nullptr);
+  const bool need_dy = a.w2t_pub == nullptr || (a.n_priv > 0 && a.tr == nullptr);
+  if (!need_xp && !need_dy) return;
   for (int c = tid; c < nch; c += BT) {
     const u32x4 gv = *(const u32x4*)(G + c * 8);
     const u32x4 xv = *(const u32x4*)(xt + c * 8);
@@ -123,7 +131,7 @@ __global__ __launch_bounds__(BT) void bwd_rows_kernel(BwdArgs a) {
       for (int q = 0; q < 4; ++q)
         o[q] = pack_bf16x2(g * bf16_to_f32(gv[q] & 0xFFFFu), g * bf16_to_f32(gv[q] >> 16));
       const size_t r = (size_t)s_row[j];
-      *(u32x4*)(a.dY + r * H + c * 8) = o;
+      if (need_dy) *(u32x4*)(a.dY + r * H + c * 8) = o;
       if (need_xp) *(u32x4*)(a.Xp + r * H + c * 8) = xv;
     }
   }
@@ -369,7 +377,8 @@ __global__ __launch_bounds__(BT) void bwd_gemm_kernel(GemmArgs p) {
 // ---------------------------------------------------------------------------
 // Reductions
 // ---------------------------------------------------------------------------
-// SwiGLU backward on the rows of dh (NT path): da = dh b s (1 + a (1 - s)),
+// SwiGLU backward on the rows of dh (NT path, where dH[r] = dout[t] W2^T and the row's
+// upstream is g_row[r] dH[r]): da = dh b s (1 + a (1 - s)),
 // db = dh a s, h = a s b, with [a; b] the saved fp32 gate and up projections; four
 // columns per thread. With pub_only, block r stops at the first private row (the private
 // rows' tile pass writes theirs together with their K-contiguous copies) and h is not
@@ -378,6 +387,7 @@ __global__ __launch_bounds__(BT) void bwd_swiglu_kernel(BwdArgs a, const float* 
   const int r = blockIdx.x, I = a.I;
   if (pub_only && r >= a.offset[a.n_pub]) return;
   const uint16_t* dh = a.dH + (size_t)r * I;
+  const float gr = a.g_row[r];  // dh here is dout W2^T; the row's upstream is g_row[r] times it
   const float* ab = AB + (size_t)r * 2 * I;
   uint16_t* da = a.dA13 + (size_t)r * 2 * I;
   uint16_t* hh = a.Hh + (size_t)r * I;
@@ -388,7 +398,7 @@ __global__ __launch_bounds__(BT) void bwd_swiglu_kernel(BwdArgs a, const float* 
     float dga[4], dub[4], h[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      swiglu_bwd(bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu), g[j], u[j], dga[j], dub[j], h[j]);
+      swiglu_bwd(gr * bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu), g[j], u[j], dga[j], dub[j], h[j]);
     *(u32x2*)(da + i) = u32x2{pack_bf16x2(dga[0], dga[1]), pack_bf16x2(dga[2], dga[3])};
     *(u32x2*)(da + I + i) = u32x2{pack_bf16x2(dub[0], dub[1]), pack_bf16x2(dub[2], dub[3])};
     if (!pub_only) *(u32x2*)(hh + i) = u32x2{pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3])};
@@ -675,9 +685,11 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     f.H = I; f.I = H;  // N = I, K = H
     f.w13_pub = f.w2_pub = a.w2t_pub;
     f.w13_priv = f.w2_priv = a.w2t_priv;
-    f.h = (void*)a.dY;
+    f.x = a.dout;  // row r reads dout[row_token[r]]; its gate is applied in the SwiGLU pass
+    f.gather_a = 1;
     f.y_perm = a.dH;
     e = launch_grouped_nt_gemm(f, s);
+    f.gather_a = 0;
     if (e != hipSuccess) return e;
     // with K-contiguous private copies, the private rows go through the tile pass that
     // also writes [da; db] and h transposed for the weight gradients
@@ -685,8 +697,8 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     bwd_swiglu_kernel<<<R, BT, 0, s>>>(a, AB, priv_t ? 1 : 0);
     e = hipGetLastError();
     if (e == hipSuccess && priv_t)
-      e = launch_swiglu_priv_t(a.dH, AB, a.dA13, a.tr, a.tr + (size_t)2 * I * a.P, R, I, a.P, a.count,
-                               a.offset, a.n_pub, a.n_priv, s);
+      e = launch_swiglu_priv_t(a.dH, a.g_row, AB, a.dA13, a.tr, a.tr + (size_t)2 * I * a.P, R, I, a.P,
+                               a.count, a.offset, a.n_pub, a.n_priv, s);
     if (e != hipSuccess) return e;
     f.H = H; f.I = 2 * I;  // N = H, K = 2I
     f.w13_pub = f.w2_pub = a.w13t_pub;
@@ -721,15 +733,24 @@ hipError_t launch_backward(const BwdArgs& a, hipStream_t s) {
     uint16_t* hT = a.tr + (size_t)2 * I * a.P;
     uint16_t* cT = a.tr + (size_t)3 * I * a.P;
     if (!a.w2t_pub) {
-      e = launch_transpose_priv(a.dA13, nullptr, daT, R, 2 * I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
-      if (e == hipSuccess) e = launch_transpose_priv(a.Hh, nullptr, hT, R, I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+      e = launch_transpose_priv(a.dA13, nullptr, nullptr, daT, R, 2 * I, a.P, a.count, a.offset, a.n_pub,
+                                a.n_priv, s);
+      if (e == hipSuccess)
+        e = launch_transpose_priv(a.Hh, nullptr, nullptr, hT, R, I, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
       if (e != hipSuccess) return e;
     }
     // dW13[p] = [da; db]^T X over private expert p's rows (x gathered by token): M = 2I, N = H
-    e = launch_transpose_priv(a.x, a.row_token, cT, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    e = launch_transpose_priv(a.x, a.row_token, nullptr, cT, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
     if (e == hipSuccess) e = launch_wgrad(WgradArgs{2 * I, H, a.P, a.n_pub, a.n_priv, daT, cT, a.count, a.dw13_priv}, s);
-    // dW2[p] = dY^T h: M = H, N = I
-    if (e == hipSuccess) e = launch_transpose_priv(a.dY, nullptr, cT, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    // dW2[p] = dY^T h: M = H, N = I; dY rows are bf16(g_row[r] dout[t]), made here from dout
+    // on the NT path (the transposing path stored them)
+    if (e == hipSuccess) {
+      if (a.w2t_pub)
+        e = launch_transpose_priv(a.dout, a.row_token, a.g_row, cT, R, H, a.P, a.count, a.offset, a.n_pub,
+                                  a.n_priv, s);
+      else
+        e = launch_transpose_priv(a.dY, nullptr, nullptr, cT, R, H, a.P, a.count, a.offset, a.n_pub, a.n_priv, s);
+    }
     if (e == hipSuccess) e = launch_wgrad(WgradArgs{H, I, a.P, a.n_pub, a.n_priv, cT, hT, a.count, a.dw2_priv}, s);
     if (e != hipSuccess) return e;
   } else if (a.n_priv > 0) {

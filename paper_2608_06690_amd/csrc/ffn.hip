@@ -128,8 +128,11 @@ struct TileInfo {
 // row into ab_save [T*k, 2I], for a later backward pass. AUDIT (GEMM2 only): count the
 // executed private rows; off when the kernel serves as a plain grouped GEMM (the
 // backward's products with transposed weights).
-template <class C, bool GATED, bool SAVE = false, bool AUDIT = true>
+// GATHER_A (GEMM2 form only): the A rows are gathered by token, row r of the product
+// reading x[row_token[r]] (the backward's dh takes the upstream gradient rows so).
+template <class C, bool GATED, bool SAVE = false, bool AUDIT = true, bool GATHER_A = false>
 __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
+  static_assert(!(GATED && GATHER_A), "GEMM1 gathers through x_perm == NULL");
   __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS];
   // Gather-index slices (row_token) of the tiles in flight. The producer runs up to
   // STAGES-1 K steps ahead of the consumer and fetches a tile's slice one tile before its
@@ -235,7 +238,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   // Does tile t read row_token? (gathered x rows in GEMM1; the audit in GEMM2)
   auto needs_rt = [&](const TileInfo& t) {
     if (t.g >= E) return false;
-    return GATED ? (a.x_perm == nullptr) : (AUDIT && t.g >= a.n_pub);
+    return GATED ? (a.x_perm == nullptr) : (GATHER_A || (AUDIT && t.g >= a.n_pub));
   };
   const uint32_t lds0 = lds_addr(smem);
   const uint32_t rt0 = lds_addr(&s_rt[0][0]);
@@ -286,7 +289,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
     if (GATED)
       baseA = (const uint16_t*)((!shared && a.x_perm) ? a.x_perm : a.x);
     else
-      baseA = (const uint16_t*)(shared ? a.h_sh : a.h);
+      baseA = (const uint16_t*)(GATHER_A ? a.x : shared ? a.h_sh : a.h);
     baseB = w;
 #pragma unroll
     for (int i = 0; i < C::A_DMA; ++i) {
@@ -298,6 +301,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
           row = (uint32_t)(t.base + rr) * (uint32_t)H;
         else
           row = (uint32_t)s_rt[slot][rr] * (uint32_t)H;
+      } else if (GATHER_A) {
+        row = (uint32_t)s_rt[slot][rr] * (uint32_t)I;
       } else {
         row = (uint32_t)(t.base + rr) * (uint32_t)I;
       }
@@ -861,7 +866,8 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t s) {
 }
 
 // The GEMM2 kernel as a plain grouped product without the audit: y[r] = h[r] W_g^T for the
-// rows of every routed group g, W_g [H, I] (K = I contiguous), bf16 in and out.
+// rows of every routed group g, W_g [H, I] (K = I contiguous), bf16 in and out. With
+// a.gather_a, row r of the product reads x[row_token[r]] (x [T, I]) instead of h[r].
 hipError_t launch_grouped_nt_gemm(const FfnArgs& a, hipStream_t s) {
   const int E = a.n_pub + a.n_priv;
   int dev = 0, ncu = 256;
@@ -875,7 +881,10 @@ hipError_t launch_grouped_nt_gemm(const FfnArgs& a, hipStream_t s) {
     int64_t tiles = ((int64_t)a.T * a.k / C::BM + E) * ((a.H + C::BN - 1) / C::BN);
     int64_t g = (int64_t)ncu * C::PER_CU;
     if (tiles < g) g = (tiles + 7) / 8 * 8;
-    hipLaunchKernelGGL((gemm_bf16_kernel<C, false, false, false>), dim3((unsigned)g), dim3(C::THREADS), 0, s, a);
+    if (a.gather_a)
+      hipLaunchKernelGGL((gemm_bf16_kernel<C, false, false, false, true>), dim3((unsigned)g), dim3(C::THREADS), 0, s, a);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<C, false, false, false>), dim3((unsigned)g), dim3(C::THREADS), 0, s, a);
   };
   if (large)
     run(CfgLarge{});

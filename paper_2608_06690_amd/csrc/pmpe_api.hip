@@ -74,9 +74,9 @@ size_t ffn_ws(const pmpe_layer_desc* d, int32_t T) {
 
 pmpe_status launched(hipError_t e) { return e == hipSuccess ? PMPE_OK : PMPE_ERR_LAUNCH; }
 
-// backward workspace: Xp, dY, [a; b], h, [da; db], row input gradients, row dz
+// backward workspace: Xp, dY, [a; b], h, [da; db], row input gradients, row dz and gates
 struct BwdLayout {
-  size_t xp, dy, ab, hh, da, dxr, dz, part, dzp, absh, dash, dxsh, dh, tr, total;
+  size_t xp, dy, ab, hh, da, dxr, dz, grow, part, dzp, absh, dash, dxsh, dh, tr, total;
   int P;  // row stride of the transposed private rows (0: weight gradients on the transposing GEMM)
 };
 int bwd_pool_stride(const pmpe_layer_desc* d) {
@@ -94,6 +94,7 @@ BwdLayout bwd_layout(const pmpe_layer_desc* d, int32_t T) {
   L.da = o; o += round_up(R * 2 * I * 2);
   L.dxr = o; o += round_up(R * H * 4);
   L.dz = o; o += round_up(R * 4);
+  L.grow = o; o += round_up(R * 4);
   L.part = o; o += round_up((size_t)d->n_priv * BWD_DWR_SPLIT * H * 4);
   const size_t Tt = (size_t)T, Is = (size_t)d->n_shared * d->shared_inter;
   L.dzp = o; o += d->gate_mode == PMPE_GATE_POOL_SOFTMAX ? round_up(Tt * bwd_pool_stride(d) * 4) : 0;
@@ -470,7 +471,7 @@ pmpe_status pmpe_backward(const pmpe_layer_desc* d, int32_t T, const void* x, co
             (float*)(w + L.absh), (uint16_t*)(w + L.dash),
             d->n_shared > 0 ? (float*)(w + L.dxsh) : nullptr,
             any_t ? w2t_pub : nullptr, w13t_pub, w2t_priv, w13t_priv, (uint16_t*)(w + L.dh),
-            L.P > 0 ? (uint16_t*)(w + L.tr) : nullptr, L.P};
+            L.P > 0 ? (uint16_t*)(w + L.tr) : nullptr, L.P, (float*)(w + L.grow)};
   return launched(launch_backward(a, (hipStream_t)stream));
 }
 

@@ -155,6 +155,7 @@ struct FfnArgs {
   const float* w2_scale_pub = nullptr;
   const float* w13_scale_priv = nullptr;
   const float* w2_scale_priv = nullptr;
+  int gather_a = 0;  // plain grouped product (launch_grouped_nt_gemm): A row r is x[row_token[r]]
 };
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn_parts(const FfnArgs& a, hipStream_t s, int parts);
@@ -249,7 +250,7 @@ struct BwdArgs {
   uint32_t* grad_rows;
   // workspace
   uint16_t* Xp;    // [T*k, H]
-  uint16_t* dY;    // [T*k, H]
+  uint16_t* dY;    // [T*k, H] (written only where a later pass reads it)
   float* AB;       // [T*k, 2I]
   uint16_t* Hh;    // [T*k, I]
   uint16_t* dA13;  // [T*k, 2I]
@@ -278,22 +279,25 @@ struct BwdArgs {
   // the weight gradients then run on the transposing GEMM
   uint16_t* tr;
   int P;
+  float* g_row;           // [T*k]: the gate of each row (its upstream rows are g_row[r] dout[t])
 };
 constexpr int BWD_DWR_SPLIT = 16;  // row chunks per private expert in the router-row gradient
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t s);
 hipError_t launch_transpose(const void* src, void* dst, int n, int rows, int cols, hipStream_t s);
 // dst [cols, P]: the private rows of src transposed and zero-padded per expert (src [rows,
-// cols] in permuted row order, or [T, cols] read through row_token when that is not NULL).
-hipError_t launch_transpose_priv(const void* src, const int32_t* row_token, void* dst, int rows_max,
-                                 int cols, int P, const int32_t* count, const int32_t* offset,
-                                 int n_pub, int n_priv, hipStream_t s);
-// SwiGLU backward of the private rows of dH [rows, I] with [a; b] from AB [rows, 2I]: [da; db]
-// into dA13 [rows, 2I] and, transposed and padded like launch_transpose_priv, into daT
-// [2I, P]; h into hT [I, P].
-hipError_t launch_swiglu_priv_t(const uint16_t* dH, const float* AB, uint16_t* dA13, uint16_t* daT,
-                                uint16_t* hT, int rows_max, int I, int P, const int32_t* count,
-                                const int32_t* offset, int n_pub, int n_priv, hipStream_t s);
+// cols] in permuted row order, or [T, cols] read through row_token when that is not NULL);
+// with row_scale, element (r, c) is bf16(row_scale[r] * src value).
+hipError_t launch_transpose_priv(const void* src, const int32_t* row_token, const float* row_scale,
+                                 void* dst, int rows_max, int cols, int P, const int32_t* count,
+                                 const int32_t* offset, int n_pub, int n_priv, hipStream_t s);
+// SwiGLU backward of the private rows of dH [rows, I] (row r's upstream gradient is
+// g_row[r] * dH[r]) with [a; b] from AB [rows, 2I]: [da; db] into dA13 [rows, 2I] and,
+// transposed and padded like launch_transpose_priv, into daT [2I, P]; h into hT [I, P].
+hipError_t launch_swiglu_priv_t(const uint16_t* dH, const float* g_row, const float* AB, uint16_t* dA13,
+                                uint16_t* daT, uint16_t* hT, int rows_max, int I, int P,
+                                const int32_t* count, const int32_t* offset, int n_pub, int n_priv,
+                                hipStream_t s);
 
 // Weight gradients of the private experts on MFMA from K-contiguous operands:
 // C[p] [M, N] fp32 = sum over the padded rows j of private expert p of AT[m][po_p + j] *

@@ -37,8 +37,15 @@ __device__ __forceinline__ u32x4 pt_get(const PairTile& t, int c, int ch) {
 // Thread (m, q) loads 16 bytes of rows 2m and 2m + 1 per tile (8 lanes per 128-byte row
 // segment), every load of the NC tiles issued before the first LDS write; the stores go
 // out as 16-byte chunks, 8 lanes per 128-byte dst row segment.
-template <int NC, class RowPtr>
-__device__ __forceinline__ void tile_transpose(RowPtr row_ptr, uint16_t* __restrict__ dst,
+// With a row scale (row_scale(r) != nullptr), element (r, c) becomes bf16(scale * value).
+__device__ __forceinline__ u32x4 scale_bf16x8(const u32x4& v, float g) {
+  u32x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(g * bf16_to_f32(v[e] & 0xFFFFu), g * bf16_to_f32(v[e] >> 16));
+  return o;
+}
+template <int NC, class RowPtr, class RowScale>
+__device__ __forceinline__ void tile_transpose(RowPtr row_ptr, RowScale row_scale, uint16_t* __restrict__ dst,
                                                size_t ld_dst) {
   __shared__ __attribute__((aligned(16))) PairTile tile[NC];
   const int tid = threadIdx.x, m = tid >> 3, q = tid & 7;
@@ -49,6 +56,18 @@ __device__ __forceinline__ void tile_transpose(RowPtr row_ptr, uint16_t* __restr
   for (int n = 0; n < NC; ++n) {
     lo[n] = s0 ? *(const u32x4*)(s0 + n * TT + q * 8) : u32x4{0, 0, 0, 0};
     hi[n] = s1 ? *(const u32x4*)(s1 + n * TT + q * 8) : u32x4{0, 0, 0, 0};
+  }
+  const float* g0 = row_scale(2 * m);
+  const float* g1 = row_scale(2 * m + 1);
+  if (g0) {
+    const float f = *g0;
+#pragma unroll
+    for (int n = 0; n < NC; ++n) lo[n] = scale_bf16x8(lo[n], f);
+  }
+  if (g1) {
+    const float f = *g1;
+#pragma unroll
+    for (int n = 0; n < NC; ++n) hi[n] = scale_bf16x8(hi[n], f);
   }
 #pragma unroll
   for (int n = 0; n < NC; ++n) pt_put(tile[n], m, q, lo[n], hi[n]);
@@ -70,7 +89,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
   const uint16_t* s = src + (size_t)blockIdx.z * mat;
   uint16_t* d = dst + (size_t)blockIdx.z * mat;
   const int r0 = blockIdx.y * TT, c0 = blockIdx.x * TT;
-  tile_transpose<1>([&](int r) { return s + (size_t)(r0 + r) * cols + c0; }, d + (size_t)c0 * rows + r0,
+  tile_transpose<1>([&](int r) { return s + (size_t)(r0 + r) * cols + c0; },
+                    [](int) -> const float* { return nullptr; }, d + (size_t)c0 * rows + r0,
                  (size_t)rows);
 }
 
@@ -117,11 +137,12 @@ __device__ bool priv_tile(const int32_t* count, const int32_t* offset, int n_pub
 
 // dst [cols, P] = the private rows of src [rows, cols], transposed and padded. With
 // row_token, src is [T, cols] indexed by token: permuted row r reads src[row_token[r]]
-// (the gathered rows are never stored row by row). One block per 64 padded rows (x) x
-// 64 NC columns (y).
+// (the gathered rows are never stored row by row); with row_scale, element (r, c) is
+// bf16(row_scale[r] * value). One block per 64 padded rows (x) x 64 NC columns (y).
 template <int NC>
 __global__ __launch_bounds__(256) void transpose_priv_kernel(const uint16_t* __restrict__ src,
                                                               const int32_t* __restrict__ row_token,
+                                                              const float* __restrict__ row_scale,
                                                               uint16_t* __restrict__ dst, int cols,
                                                               int P, const int32_t* count,
                                                               const int32_t* offset, int n_pub,
@@ -133,16 +154,20 @@ __global__ __launch_bounds__(256) void transpose_priv_kernel(const uint16_t* __r
     if (pt.jl + r >= pt.cnt) return nullptr;
     const int row = row_token ? row_token[pt.src0 + r] : pt.src0 + r;
     return src + (size_t)row * cols + c0;
+  }, [&](int r) -> const float* {
+    return (row_scale && pt.jl + r < pt.cnt) ? row_scale + pt.src0 + r : nullptr;
   }, dst + (size_t)c0 * P + pt.j0, (size_t)P);
 }
 
-// SwiGLU backward of the private rows (the rows of the NT backward's dh, I columns), with
+// SwiGLU backward of the private rows (the rows of the NT backward's dh, I columns, whose
+// upstream gradient is g_row[r] * dH[r]), with
 // their outputs in both layouts: [da; db] row by row into dA13 [rows, 2I] (the row input
 // gradients read them so), and K contiguous into daT [2I, P] (da in rows 0..I-1, db in
 // rows I..2I-1) and h into hT [I, P] for the weight gradients. Block: 64 padded rows (x)
 // x 64 columns (y); each thread computes 8 columns of two rows, and the three tiles go out
 // transposed through LDS. Padding columns get zeros.
 __global__ __launch_bounds__(256) void swiglu_priv_t_kernel(const uint16_t* __restrict__ dH,
+                                                             const float* __restrict__ g_row,
                                                              const float* __restrict__ AB,
                                                              uint16_t* __restrict__ dA13,
                                                              uint16_t* __restrict__ daT,
@@ -162,6 +187,7 @@ __global__ __launch_bounds__(256) void swiglu_priv_t_kernel(const uint16_t* __re
     if (pt.jl + r < pt.cnt) {
       const size_t row = (size_t)(pt.src0 + r);
       const u32x4 dv = *(const u32x4*)(dH + row * I + c0 + q * 8);
+      const float gr = g_row[row];
       const float* g = AB + row * 2 * I + c0 + q * 8;
       const f32x4 g0 = *(const f32x4*)g, g1 = *(const f32x4*)(g + 4);
       const f32x4 u0 = *(const f32x4*)(g + I), u1 = *(const f32x4*)(g + I + 4);
@@ -170,7 +196,7 @@ __global__ __launch_bounds__(256) void swiglu_priv_t_kernel(const uint16_t* __re
       float da[8], db[8], h[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        swiglu_bwd(bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu), gg[j], uu[j], da[j], db[j], h[j]);
+        swiglu_bwd(gr * bf16_to_f32(j & 1 ? dv[j >> 1] >> 16 : dv[j >> 1] & 0xFFFFu), gg[j], uu[j], da[j], db[j], h[j]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         oa[v][e] = pack_bf16x2(da[2 * e], da[2 * e + 1]);
@@ -201,28 +227,29 @@ __global__ __launch_bounds__(256) void swiglu_priv_t_kernel(const uint16_t* __re
 // padded private rows never exceed rows_max rounded up to 64, plus 64 per private expert
 static int priv_xtiles(int rows_max, int n_priv) { return (rows_max + TT - 1) / TT + n_priv; }
 
-hipError_t launch_transpose_priv(const void* src, const int32_t* row_token, void* dst, int rows_max,
-                                 int cols, int P, const int32_t* count, const int32_t* offset,
-                                 int n_pub, int n_priv, hipStream_t s) {
+hipError_t launch_transpose_priv(const void* src, const int32_t* row_token, const float* row_scale,
+                                 void* dst, int rows_max, int cols, int P, const int32_t* count,
+                                 const int32_t* offset, int n_pub, int n_priv, hipStream_t s) {
   // four 64 x 64 tiles per block where the columns allow (more loads in flight per block)
   const int nc = cols % (4 * TT) == 0 ? 4 : cols % (2 * TT) == 0 ? 2 : 1;
   const dim3 grid(priv_xtiles(rows_max, n_priv), cols / (TT * nc));
   const uint16_t* in = (const uint16_t*)src;
   uint16_t* out = (uint16_t*)dst;
   if (nc == 4)
-    transpose_priv_kernel<4><<<grid, 256, 0, s>>>(in, row_token, out, cols, P, count, offset, n_pub, n_priv);
+    transpose_priv_kernel<4><<<grid, 256, 0, s>>>(in, row_token, row_scale, out, cols, P, count, offset, n_pub, n_priv);
   else if (nc == 2)
-    transpose_priv_kernel<2><<<grid, 256, 0, s>>>(in, row_token, out, cols, P, count, offset, n_pub, n_priv);
+    transpose_priv_kernel<2><<<grid, 256, 0, s>>>(in, row_token, row_scale, out, cols, P, count, offset, n_pub, n_priv);
   else
-    transpose_priv_kernel<1><<<grid, 256, 0, s>>>(in, row_token, out, cols, P, count, offset, n_pub, n_priv);
+    transpose_priv_kernel<1><<<grid, 256, 0, s>>>(in, row_token, row_scale, out, cols, P, count, offset, n_pub, n_priv);
   return hipGetLastError();
 }
 
-hipError_t launch_swiglu_priv_t(const uint16_t* dH, const float* AB, uint16_t* dA13, uint16_t* daT,
-                                uint16_t* hT, int rows_max, int I, int P, const int32_t* count,
-                                const int32_t* offset, int n_pub, int n_priv, hipStream_t s) {
+hipError_t launch_swiglu_priv_t(const uint16_t* dH, const float* g_row, const float* AB, uint16_t* dA13,
+                                uint16_t* daT, uint16_t* hT, int rows_max, int I, int P,
+                                const int32_t* count, const int32_t* offset, int n_pub, int n_priv,
+                                hipStream_t s) {
   swiglu_priv_t_kernel<<<dim3(priv_xtiles(rows_max, n_priv), I / TT), 256, 0, s>>>(
-      dH, AB, dA13, daT, hT, I, P, count, offset, n_pub, n_priv);
+      dH, g_row, AB, dA13, daT, hT, I, P, count, offset, n_pub, n_priv);
   return hipGetLastError();
 }
 
