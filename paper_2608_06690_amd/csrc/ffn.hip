@@ -9,8 +9,9 @@
 // counts, so groups with zero rows get no tile and load nothing. Tiles are numbered
 // group-major, then N tile, then M tile, so concurrent tiles share weight and row
 // tiles; block ids are remapped so that each XCD (workgroups are dealt to the 8 XCDs
-// round-robin) works on one contiguous range of that order and its L2 holds the
-// shared operands.
+// round-robin) works on one contiguous range of the routed experts' tiles and its L2
+// holds the shared operands; the shared group's tiles (longest K loop in GEMM2) are
+// spread over the XCDs ahead of them.
 //
 //   GEMM1  [rows, H] x [H, 2I]: the N tile holds BN/2 gate columns and the matching
 //          BN/2 up columns, so h = silu(g) * u is formed in registers and rounded once
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   __shared__ int s_cum[MAXG + 1];
   __shared__ int s_cnt[MAXG];
   __shared__ int s_off[MAXG];
-  // interleaved tile order (prefill tiles only: the decode tiles' two blocks per CU have no
+  // interleaved group order (prefill tiles only: the decode tiles' two blocks per CU have no
   // LDS to spare for the permutation)
   constexpr bool MIX = C::BM >= 256;
   __shared__ int s_perm[MIX ? MAXG : 1];
@@ -165,23 +166,26 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   const int TK = a.T * a.k;
 
   if (tid < 64) {
-    // Tile order, prefill tiles (256 rows): the public and the private experts interleaved
-    // in proportion to the pool sizes (public j before private p iff
-    // (2j+1) n_priv <= (2p+1) n_pub), the shared group last. Each XCD's contiguous slice of
-    // the order then holds both kinds of tiles (the private experts' full tiles carry about
-    // twice the MFMA work of the half-filled public ones), while the tiles of one expert stay
-    // adjacent (Qwen-shaped layer: -2.7 %). Decode-shaped tiles keep the expert order.
+    // Tile order, prefill tiles (256 rows): the shared group first (all T tokens; in GEMM2
+    // its K loop over 2 I_s is the longest, so its tiles must not be left for the end),
+    // then the public and the private experts interleaved in proportion to the pool sizes
+    // (public j before private p iff (2j+1) n_priv <= (2p+1) n_pub). Each XCD's slice of
+    // the routed tiles then holds both kinds (the private experts' full tiles carry about
+    // twice the MFMA work of the half-filled public ones), while the tiles of one expert
+    // stay adjacent. Decode-shaped tiles keep the expert order (their two blocks per CU
+    // have no LDS to spare for the permutation).
+    const int sh = (ngroups > E) ? 1 : 0;
     for (int g = tid; MIX && g < ngroups; g += 64) {
       int pos;
       if (g < a.n_pub) {
         const int num = (2 * g + 1) * a.n_priv;  // private experts before public g
-        pos = g + min(a.n_priv, ((num + a.n_pub - 1) / a.n_pub) / 2);
+        pos = sh + g + min(a.n_priv, ((num + a.n_pub - 1) / a.n_pub) / 2);
       } else if (g < E) {
         const int p = g - a.n_pub;
         const int f = (2 * p + 1) * a.n_pub / a.n_priv;  // public experts before private p
-        pos = p + min(a.n_pub, (f + 1) / 2);
+        pos = sh + p + min(a.n_pub, (f + 1) / 2);
       } else {
-        pos = g;
+        pos = 0;
       }
       s_perm[pos] = g;
     }
@@ -206,17 +210,30 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(FfnArgs a) {
   }
   __syncthreads();
 
-  // This block's tiles: L_i = start_x + q + i * nbx, i < ntl.
+  // Block ids are remapped so that XCD x (workgroups go to the 8 XCDs round-robin) takes
+  // one contiguous slice of the routed tiles, dealt round-robin to its blocks: tiles that
+  // share an expert's weights or rows then run on one XCD and meet in its L2. The shared
+  // group's tiles (prefill) come before them in every XCD's list, dealt to the XCDs in
+  // chunks of XCH consecutive tiles (M tiles of one weight tile), so that every XCD gets
+  // its share of them.
+  constexpr int XCH = 8;
   const int total = s_cum[ngroups];
+  const int n_sh = (MIX && ngroups > E) ? s_cum[1] : 0;  // shared tiles, first in the order
+  const int n_rt = total - n_sh;
   const int b = blockIdx.x, x = b & 7, q = b >> 3;
-  const int cnt_x = (total >> 3) + (x < (total & 7) ? 1 : 0);
   const int nbx = ((int)gridDim.x - x + 7) >> 3;
-  const int start_x = x * (total >> 3) + min(x, total & 7);
+  const int nch = (n_sh + XCH - 1) / XCH;               // chunks of shared tiles
+  const int nch_x = (nch > x) ? (nch - x + 7) / 8 : 0;  // those of XCD x
+  // the last chunk (nch - 1) is the only one that may be partial
+  const int sh_x = nch_x * XCH - ((nch_x > 0 && (nch - 1) % 8 == x) ? (nch * XCH - n_sh) : 0);
+  const int cnt_x = sh_x + (n_rt >> 3) + (x < (n_rt & 7) ? 1 : 0);
+  const int start_x = n_sh + x * (n_rt >> 3) + min(x, n_rt & 7);
   const int ntl = (cnt_x > q && q < nbx) ? (cnt_x - q + nbx - 1) / nbx : 0;
   if (ntl == 0) return;
 
   auto tile_of = [&](int i) {
-    const int L = start_x + q + i * nbx;
+    const int j = q + i * nbx;  // index within the XCD's tiles
+    const int L = (j < sh_x) ? (x + 8 * (j / XCH)) * XCH + (j % XCH) : start_x + (j - sh_x);
     int lo = 0, hi = ngroups - 1;  // last position o with s_cum[o] <= L (a group with tiles)
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
