@@ -229,10 +229,14 @@ def test_prefill_multi_tile(gather):
     assert cnt[cfg.n_pub:].min() > 2 * 256 and cnt[:cfg.n_pub].min() > 256   # ragged multi-tile experts
 
 
-def test_prefill_shared_group_pool_softmax():
-    cfg = W.scaled_config(W.get_config("deepseek"), tokens=2048, requests=4, hidden=512, inter=256,
-                          n_pub=32, n_priv=8, top_k=6, shared_inter=128)
-    assert cfg.n_shared * cfg.shared_inter == 256
+# The shared group's tiles lead every XCD's tile list in chunks of 8: 2048 tokens give 16
+# shared tiles per GEMM (whole chunks); 1300 tokens with 2 I_s = 384 give 18 (GEMM1) and 12
+# (GEMM2), each ending in a partial chunk.
+@pytest.mark.parametrize("tokens,shared_inter", [(2048, 128), (1300, 192)], ids=["whole_chunks", "partial_chunk"])
+def test_prefill_shared_group_pool_softmax(tokens, shared_inter):
+    cfg = W.scaled_config(W.get_config("deepseek"), tokens=tokens, requests=4, hidden=512, inter=256,
+                          n_pub=32, n_priv=8, top_k=6, shared_inter=shared_inter)
+    assert cfg.tokens * cfg.top_k >= 128 * (cfg.n_pub + cfg.n_priv)  # the 256 x 256 prefill tiles
     layer, _ = C.device_layer(cfg)
     x = W.make_x(cfg, "cuda")
     req, words = words_for(cfg)
