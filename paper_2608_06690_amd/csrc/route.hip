@@ -487,7 +487,8 @@ __global__ __launch_bounds__(RW_THREADS) void route_logits_wide_kernel(RouteArgs
       if (!part(tt)) continue;
       float z = acc[mb][i];
       if (split == 0 && a.bias) z += bias;
-      zp[(size_t)(t0 + tt) * a.zstride + zc] = z;
+      // non-temporal: the partial logits are read once, by the top-k kernel
+      __builtin_nontemporal_store(z, &zp[(size_t)(t0 + tt) * a.zstride + zc]);
     }
 }
 
@@ -521,23 +522,32 @@ __global__ __launch_bounds__(RT_THREADS) void route_topk_kernel(RouteArgs a) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int t = blockIdx.x * RT_WAVES + w;
   if (t >= a.T) return;  // wave-uniform; no block barrier follows
-  const int tau = token_tau(a, t);
-  // masked: the permitted pool; soft (control arm): the concatenated pool
-  const int N = a.soft ? a.n_pub + a.n_priv : (tau ? a.n_priv : a.n_pub);
-  const int base = (a.soft || !tau) ? 0 : a.n_pub;
   const float* z = a.z + (size_t)t * a.zstride;
   if (a.zsplit > 1) {
+    // the whole zstride-wide row of every split is loaded without waiting for the policy
+    // word (entries past the pool are added but never ranked), then added in split order
     const size_t pstride = (size_t)a.T * a.zstride;
-    for (int s = lane; s < N; s += 64) {
-      float v = z[s];
-      for (int p = 1; p < a.zsplit; ++p) v += z[p * pstride + s];
-      s_z[w][s] = v;
+    if (a.zsplit == 4) {
+      for (int s = lane; s < a.zstride; s += 64) {
+        const float v0 = z[s], v1 = z[pstride + s], v2 = z[2 * pstride + s], v3 = z[3 * pstride + s];
+        s_z[w][s] = ((v0 + v1) + v2) + v3;
+      }
+    } else {
+      for (int s = lane; s < a.zstride; s += 64) {
+        float v = z[s];
+        for (int p = 1; p < a.zsplit; ++p) v += z[p * pstride + s];
+        s_z[w][s] = v;
+      }
     }
     // the wave's LDS writes complete before any lane reads another lane's entry
     __builtin_amdgcn_s_waitcnt(0xc07f);
     __builtin_amdgcn_wave_barrier();
     z = &s_z[w][0];
   }
+  const int tau = token_tau(a, t);
+  // masked: the permitted pool; soft (control arm): the concatenated pool
+  const int N = a.soft ? a.n_pub + a.n_priv : (tau ? a.n_priv : a.n_pub);
+  const int base = (a.soft || !tau) ? 0 : a.n_pub;
   TopkCtx c{a.T, a.n_pub, a.n_priv, a.k, a.gate_mode, a.topk_idx, a.topk_gate, a.allow, a.kgap};
   if (N <= 64)
     topk_one_token<1>(c, t, tau, N, base, z);
