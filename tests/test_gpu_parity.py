@@ -126,6 +126,33 @@ def test_large_batch_router(shape):
     full_check(cfg, layer, x, words, req)
 
 
+# The large-batch top-k adds every split's whole partial-logit row of a token (the row is as
+# wide as the larger pool) before the token's policy word has told it which pool it ranks, so
+# entries past the pool hold whatever the workspace held. The routing must not depend on it:
+# the same batch routed over a workspace of zeros, NaNs and huge values gives the same bits.
+@pytest.mark.parametrize("soft", [False, True], ids=["masked", "soft"])
+def test_large_batch_router_ignores_workspace_contents(soft):
+    shape = dict(tokens=4100, requests=5, hidden=384, inter=128, n_pub=128, n_priv=32, top_k=8)
+    cfg = W.scaled_config(W.get_config("qwen"), **shape)
+    layer, _ = C.device_layer(cfg, soft=soft)
+    x = W.make_x(cfg, "cuda")
+    req = W.alternating_requests(cfg.requests, cfg.tokens // cfg.requests)
+    req.lengths[-1] += cfg.tokens - sum(req.lengths)
+    words = C.words_tensor(O.compile_words(req.metas, req.lengths))
+    b = layer.buffers(cfg.tokens)
+    log(f"router workspace fills: T={cfg.tokens} soft={soft}")
+    outs = []
+    for fill in (0.0, float("nan"), 3.0e38, -3.0e38):
+        b.ws.view(torch.float32).fill_(fill)
+        layer.route(x, words, b)
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in (b.topk_idx, b.topk_gate, b.allow, b.kgap)])
+    for o in outs[1:]:
+        for got, ref in zip(o, outs[0]):
+            assert torch.equal(got, ref)
+    assert int(b.dev_status.item()) == 0
+
+
 # Expert intermediate 64: the down projection has a single K step per tile, so in a
 # persistent block the copy producer runs up to STAGES-1 tiles ahead of the tile being
 # multiplied, and the gather-index (row_token) slices of STAGES+1 tiles are live at once;
