@@ -43,7 +43,7 @@ COPY_BYTES = 1 << 30
 # for a plain copy of known size). Keyed by the SHA-256 of the kernel sources the
 # counters were taken on (the GEMM and its copy helper): any other source reports null.
 FFN_TRAFFIC_BYTES = {
-    "659c2e528363bc07daa302978ae9d193bee5e74ad7afe267e88bf2cee6cee31c": 1_988_275_712,
+    "23d3c310a0ec016629cdb9c251d67b08d14b3f19f816719505763ac2b0edbf9c": 2_027_439_378,
 }
 FFN_SOURCES = ("ffn.hip", "lds_dma.h")
 

@@ -82,9 +82,13 @@ using CfgLarge = Cfg<256, 256, 4, 2, 2, 64>;  // prefill: 8 waves of 64 x 128, 2
 // decode-shaped: 4 waves, 3 x 24 KiB stages, streamed weights
 using CfgSmall = Cfg<64, 128, 1, 4, 3, 64, 2, true, true>;
 // fp8 weights: the smaller weight tiles leave room for a third stage (3 x 48 KiB) in the
-// prefill configuration and for three resident blocks per CU in the decode one
+// prefill configuration. The decode one takes 256 weight rows per tile, so that a K step
+// copies as many weight bytes (16 KiB) as the bf16 decode tile and two blocks per CU keep as
+// much of the weight stream in flight; its copies carry no non-temporal hint, because a
+// 64-byte fp8 row step reads half a line and the next step must find the other half in L2
+// (with the hint: 1.35x the weight bytes fetched from HBM).
 using CfgLarge8 = Cfg<256, 256, 4, 2, 3, 64, 1, true, false, true>;
-using CfgSmall8 = Cfg<64, 128, 1, 4, 3, 64, 2, true, true, true>;
+using CfgSmall8 = Cfg<64, 256, 1, 4, 3, 64, 2, true, false, true>;
 
 constexpr int MAXG = 2 * PMPE_MAX_POOL + 1;  // routed experts + the shared group
 
